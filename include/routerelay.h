@@ -1,0 +1,191 @@
+/*
+ * routerelay.h -- C ABI of librouterelay.so, the MI355X (gfx950) route-
+ * maintenance path of RouteRelay (arXiv 2609.07306).
+ *
+ * Problem (Sec. 2.1, Eq. (1)-(2)): per query head h, chunk representations
+ * Qc[h] in R^{n_q x d} and Kc[g] in R^{n_k x d} (g = h / (H_q / H_kv)) give
+ * scores S = Qc Kc^T, and row i routes to the k best key chunks.  RouteRelay
+ * (Sec. 3) keeps, per row, a ledger of the selected set R, m near-miss and r
+ * random sentinels C, and the layer the entry was built at.  Anchor layers
+ * rebuild every entry; intermediate (relay) layers rescore R u C, keep the
+ * route of a row when its weakest selected score beats its strongest sentinel
+ * by more than gamma, and fully reroute the other rows only (Sec. 3.2,
+ * Sec. 4.1-4.2).
+ *
+ * Conventions shared by every call:
+ *   - Tensors are DEVICE pointers owned by the caller, row-major, contiguous.
+ *     Qc is [H_q, n_q, d] and Kc is [H_kv, n_k, d], binary32 (RR_F32) or bf16
+ *     (RR_BF16, 16-bit storage).  Scores are accumulated in binary32.
+ *   - Row index: row = h * n_q + i.  The causal chunk mask lets row i select
+ *     key chunks j <= i only (needs n_q == n_k); such a row has n_i = i + 1
+ *     valid chunks, a row without the mask has n_i = n_k.
+ *   - A route is a SET, stored sorted by ascending chunk id and padded with
+ *     -1 (a row with n_i < k routes to all of its valid chunks).  Ties in
+ *     score are broken toward the lower chunk id; -0 equals +0.
+ *   - Every call enqueues work on the given HIP stream (NULL: the null
+ *     stream) and returns; outputs, including device counters, are valid once
+ *     that stream has reached the enqueued work.  No call synchronises the
+ *     host with the device and none allocates memory, except
+ *     rr_ledger_create.
+ *   - The caller keeps Qc, Kc and the output buffers alive until the stream
+ *     has passed the call.  A ledger is used by one host thread on one stream
+ *     at a time.
+ *   - Errors are reported by the return value; rr_last_error() returns a
+ *     message for the calling thread's most recent failure.  Argument errors
+ *     are detected before any work is enqueued.
+ */
+#ifndef ROUTERELAY_H
+#define ROUTERELAY_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    RR_OK = 0,
+    RR_ERR_INVALID = -1,     /* an argument or configuration value is invalid */
+    RR_ERR_OOM = -2,         /* device allocation failed */
+    RR_ERR_HIP = -3,         /* a HIP runtime call failed (message in rr_last_error) */
+    RR_ERR_STATE = -4,       /* call order violated (relay before any anchor, layer going back) */
+    RR_ERR_UNSUPPORTED = -5  /* valid but outside the shapes this build supports */
+} rr_status;
+
+typedef enum { RR_F32 = 0, RR_BF16 = 1 } rr_dtype;
+
+/* Shape and rule parameters.  Supported: d in {32, 64, 128} (and 256 for
+ * bf16); 1 <= k <= n_k; k + m <= 128; k + m + r <= 256; n_k <= 8192;
+ * n_heads a multiple of n_kv_heads; gamma not NaN.  gamma is the guard
+ * margin of Eq. (8); the paper uses gamma >= 0 (0 by default, Table 1);
+ * +INFINITY refreshes every row that has a sentinel and -INFINITY refreshes
+ * none.  seed keys the random-sentinel probes. */
+typedef struct {
+    int32_t n_heads;    /* H_q */
+    int32_t n_kv_heads; /* H_kv */
+    int32_t n_q;        /* query chunks per head */
+    int32_t n_k;        /* key chunks per head */
+    int32_t d;          /* representation width */
+    int32_t k;          /* route width */
+    int32_t m;          /* near-miss sentinels */
+    int32_t r;          /* random sentinels */
+    int32_t dtype;      /* rr_dtype of Qc and Kc */
+    int32_t causal;     /* 1: chunk mask j <= i */
+    float gamma;        /* guard margin */
+    uint32_t reserved;  /* must be 0 */
+    uint64_t seed;
+} rr_config;
+
+typedef struct rr_ledger rr_ledger;
+
+/* Route ledger (Sec. 3.1, Eq. (4); state tensors of Sec. 4.1).  Allocates,
+ * on the current HIP device, the structure-of-arrays ledger -- routes
+ * [H_q*n_q, k], sentinels [H_q*n_q, m+r] (near-miss slots first, sorted by
+ * id; then random slots in draw order; -1 padded), build layer and age
+ * [H_q*n_q] int32 -- plus the per-row scratch of the relay path.  *out
+ * receives the handle (NULL on failure).  Returns RR_ERR_INVALID /
+ * RR_ERR_UNSUPPORTED for a bad config, RR_ERR_OOM if allocation fails. */
+rr_status rr_ledger_create(const rr_config *cfg, rr_ledger **out);
+
+/* Frees the ledger's device memory after synchronising the device.  NULL is
+ * a no-op. */
+rr_status rr_ledger_destroy(rr_ledger *ledger);
+
+/* Anchor layer (Sec. 3.1; forced anchors, Sec. 3.2): full routing of every
+ * row (Eq. (1)-(2)) that also keeps the chunks ranked k+1..k+m as near-miss
+ * sentinels and draws r random sentinels from the remaining valid chunks;
+ * every ledger entry is rebuilt with build layer = layer and age 0.
+ *   layer   >= 0; it keys the random probes.  An anchor may restart the layer
+ *           sequence (a new forward pass): later relays must not go below it.
+ *   Qc, Kc  device inputs as above.
+ *   routes  optional device output [H_q*n_q, k] int32 (a copy of the ledger's
+ *           routes); may be NULL.
+ *   pairs   optional device int64: number of scores evaluated (sum of n_i).
+ */
+rr_status rr_anchor_route(rr_ledger *ledger, int32_t layer, const void *Qc, const void *Kc,
+                          int32_t *routes, int64_t *pairs, void *hip_stream);
+
+/* Relay layer (Sec. 3.2, Eq. (5)-(8); dataflow of Sec. 4.1-4.2).  Each row
+ * rescores its candidates A = R u C at this layer: alpha = min over R,
+ * beta = max over C.  A row with a non-empty C and beta + gamma >= alpha is
+ * rerouted: its full score row is computed and its ledger entry rebuilt as at
+ * an anchor (build layer = layer, age 0).  Other rows keep their entry and get
+ * age = layer - build layer.  The rerouted rows are compacted per head and
+ * only they run the GEMM + TopK; with none, that step does no work.
+ *   routes      optional device output [H_q*n_q, k] int32 (copy of the
+ *               ledger's routes after the update); NULL to read the ledger
+ *               through rr_ledger_routes instead.
+ *   mask        optional device output [H_q*n_q] uint8: 1 = rerouted.
+ *   pairs       optional device int64: scores evaluated, i.e. the sum over
+ *               rows of |A_i| (valid candidate slots) plus n_i per rerouted
+ *               row.
+ *   n_rerouted  optional device int32: number of rerouted rows.
+ * Returns RR_ERR_STATE if no anchor (or import) preceded it or if layer is
+ * below the previous call's layer. */
+rr_status rr_relay_layer(rr_ledger *ledger, int32_t layer, const void *Qc, const void *Kc,
+                         int32_t *routes, uint8_t *mask, int64_t *pairs, int32_t *n_rerouted,
+                         void *hip_stream);
+
+/* Full routing baseline (Eq. (1)-(2)) with the same GEMM + TopK kernels and
+ * no ledger: routes [H_q*n_q, cfg->k] int32 receives every row's route.
+ * cfg->m and cfg->r are ignored.  route_scores (optional, [H_q*n_q, k]
+ * binary32) receives the score of each route slot (padding: -INFINITY).
+ * pairs (optional device int64) receives the number of scores evaluated. */
+rr_status rr_full_route(const rr_config *cfg, const void *Qc, const void *Kc, int32_t *routes,
+                        float *route_scores, int64_t *pairs, void *hip_stream);
+
+/* Borrowed device view of the ledger's routes [H_q*n_q, k]; valid until the
+ * next call that mutates or destroys the ledger.  NULL for a NULL ledger. */
+const int32_t *rr_ledger_routes(const rr_ledger *ledger);
+
+/* Copies the ledger state into caller device buffers (each may be NULL):
+ * routes [rows,k], sent [rows,m+r], build [rows], age [rows] int32. */
+rr_status rr_ledger_export(const rr_ledger *ledger, int32_t *routes, int32_t *sent,
+                           int32_t *build, int32_t *age, void *hip_stream);
+
+/* Replaces the ledger state from caller device buffers (all four required)
+ * and records `layer` as the last layer seen, so that a relay may follow.
+ * The contents are trusted: ids must lie in [-1, n_i) with R sorted. */
+rr_status rr_ledger_import(rr_ledger *ledger, int32_t layer, const int32_t *routes,
+                           const int32_t *sent, const int32_t *build, const int32_t *age,
+                           void *hip_stream);
+
+/* Diagnostics of the most recent relay: per-row alpha and beta (binary32,
+ * beta = -INFINITY for an empty C) and the compacted rerouted row ids, one
+ * ascending list per head at ids[h*n_q .. h*n_q + count_h).  Each output
+ * may be NULL. */
+rr_status rr_ledger_relay_stats(const rr_ledger *ledger, float *alpha, float *beta,
+                                int32_t *ids, void *hip_stream);
+
+/* Kernel timing for measurement.  Between rr_profile_start and
+ * rr_profile_stop every kernel the library launches is bracketed by HIP
+ * events recorded on its own stream.  rr_profile_stop waits for those events
+ * and returns, per kernel kind, the summed duration in milliseconds and the
+ * number of launches (arrays of RR_KERNEL_KINDS entries, each may be NULL).
+ * Process-wide; not for concurrent use from several threads. */
+typedef enum {
+    RR_KERNEL_FULL = 0,     /* GEMM + TopK, full routing */
+    RR_KERNEL_ANCHOR = 1,   /* GEMM + TopK + ledger build, every row */
+    RR_KERNEL_REROUTE = 2,  /* GEMM + TopK + ledger build, compacted rows */
+    RR_KERNEL_RESCORE = 3,  /* gather-dot, trigger, compaction counts, ages */
+    RR_KERNEL_KINDS = 4
+} rr_kernel_kind;
+
+rr_status rr_profile_start(void);
+rr_status rr_profile_stop(double *total_ms, int64_t *launches);
+
+/* Number of bytes of ledger index storage (routes plus sentinels) for a
+ * config: H_q * n_q * (k + m + r) * 4. */
+size_t rr_ledger_index_bytes(const rr_config *cfg);
+
+const char *rr_status_string(rr_status status);
+
+/* Message of the calling thread's most recent failure ("" if none). */
+const char *rr_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ROUTERELAY_H */

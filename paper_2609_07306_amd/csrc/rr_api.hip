@@ -1,0 +1,468 @@
+// Host side of the C ABI declared in include/routerelay.h: configuration
+// checks, the ledger's device allocations, and stream-ordered launches of the
+// route (GEMM + TopK) and rescoring kernels.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "routerelay.h"
+#include "rr_internal.hpp"
+
+struct rr_ledger {
+    rr_config cfg;
+    int device;
+    bool has_state;
+    int32_t last_layer;
+    int64_t rows;
+    int32_t *routes, *sent, *build, *age, *ids, *tile_base, *stat_nrr;
+    uint8_t *flags;
+    float *alpha, *beta, *theta;
+    unsigned long long *acc_pairs;
+    uint32_t *acc_count, *ticket;
+    int64_t *stat_pairs;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+rr_status fail(rr_status s, const std::string &msg)
+{
+    g_err = msg;
+    return s;
+}
+
+rr_status hip_fail(hipError_t e, const char *what)
+{
+    return fail(RR_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+int64_t rows_of(const rr_config &c) { return (int64_t)c.n_heads * c.n_q; }
+
+// Sum of n_i over all rows: the score pairs of one full routing pass.
+int64_t full_pairs(const rr_config &c)
+{
+    if (!c.causal) return rows_of(c) * c.n_k;
+    int64_t per_head = 0;
+    for (int64_t i = 0; i < c.n_q; ++i) per_head += (i + 1 < c.n_k) ? i + 1 : c.n_k;
+    return per_head * c.n_heads;
+}
+
+rr_status validate(const rr_config *c, bool ledger)
+{
+    if (!c) return fail(RR_ERR_INVALID, "config is NULL");
+    if (c->reserved != 0) return fail(RR_ERR_INVALID, "config.reserved must be 0");
+    if (c->n_heads < 1 || c->n_kv_heads < 1 || c->n_heads % c->n_kv_heads != 0)
+        return fail(RR_ERR_INVALID, "n_heads must be a positive multiple of n_kv_heads");
+    if (c->n_q < 1 || c->n_k < 1) return fail(RR_ERR_INVALID, "n_q and n_k must be >= 1");
+    if (c->causal != 0 && c->causal != 1) return fail(RR_ERR_INVALID, "causal must be 0 or 1");
+    if (c->causal && c->n_q != c->n_k) return fail(RR_ERR_INVALID, "the causal chunk mask needs n_q == n_k");
+    if (c->dtype != RR_F32 && c->dtype != RR_BF16) return fail(RR_ERR_INVALID, "dtype must be RR_F32 or RR_BF16");
+    if (c->d < 1) return fail(RR_ERR_INVALID, "d must be >= 1");
+    if (c->k < 1 || c->k > c->n_k) return fail(RR_ERR_INVALID, "k must lie in [1, n_k]");
+    if (c->m < 0 || c->r < 0) return fail(RR_ERR_INVALID, "m and r must be >= 0");
+    if (std::isnan(c->gamma)) return fail(RR_ERR_INVALID, "gamma is NaN");
+    const int m = ledger ? c->m : 0, r = ledger ? c->r : 0;
+    if (!rr::route_supported(c->dtype, c->d, c->k + m))
+        return fail(RR_ERR_UNSUPPORTED, "unsupported (dtype, d, k+m): d in {32,64,128} (256 for bf16), k+m <= 128");
+    if (c->k + m + r > 256) return fail(RR_ERR_UNSUPPORTED, "k + m + r must be <= 256");
+    if (c->n_k > 8192) return fail(RR_ERR_UNSUPPORTED, "n_k must be <= 8192");
+    if (rows_of(*c) * (int64_t)(c->k + m + r + 1) >= (int64_t)INT32_MAX || rows_of(*c) * c->d >= (int64_t)INT32_MAX * 8)
+        return fail(RR_ERR_UNSUPPORTED, "problem too large for 32-bit row indexing");
+    return RR_OK;
+}
+
+// Makes the ledger's device current for the lifetime of the guard.
+struct DeviceGuard {
+    int prev = -1;
+    bool changed = false;
+    explicit DeviceGuard(int dev)
+    {
+        if (hipGetDevice(&prev) == hipSuccess && prev != dev) changed = (hipSetDevice(dev) == hipSuccess);
+    }
+    ~DeviceGuard()
+    {
+        if (changed) (void)hipSetDevice(prev);
+    }
+};
+
+template <typename T>
+rr_status alloc(T **p, int64_t n, const char *what)
+{
+    *p = nullptr;
+    hipError_t e = hipMalloc(reinterpret_cast<void **>(p), (size_t)(n > 0 ? n : 1) * sizeof(T));
+    if (e != hipSuccess) {
+        *p = nullptr;
+        (void)hipGetLastError();
+        return fail(RR_ERR_OOM, std::string("hipMalloc failed for ") + what);
+    }
+    return RR_OK;
+}
+
+void free_all(rr_ledger *L)
+{
+    void *ptrs[] = {L->routes, L->sent,  L->build, L->age,       L->ids,       L->tile_base,
+                    L->stat_nrr, L->flags, L->alpha, L->beta, L->theta, L->acc_pairs,
+                    L->acc_count, L->ticket, L->stat_pairs};
+    for (void *p : ptrs)
+        if (p) (void)hipFree(p);
+}
+
+// ------------------------------------------------------------ profiling
+
+struct ProfRecord {
+    int kind;
+    hipEvent_t start, stop;
+};
+
+struct Profiler {
+    bool on = false;
+    std::vector<ProfRecord> records;
+    std::vector<hipEvent_t> pool;
+
+    hipEvent_t get()
+    {
+        if (!pool.empty()) {
+            hipEvent_t e = pool.back();
+            pool.pop_back();
+            return e;
+        }
+        hipEvent_t e = nullptr;
+        if (hipEventCreate(&e) != hipSuccess) return nullptr;
+        return e;
+    }
+};
+
+Profiler g_prof;
+
+// Launches `fn` on `stream`, bracketed by events when profiling is on.
+template <typename F>
+hipError_t timed(int kind, hipStream_t stream, F fn)
+{
+    if (!g_prof.on) return fn();
+    ProfRecord rec{kind, g_prof.get(), g_prof.get()};
+    if (!rec.start || !rec.stop) return fn();
+    hipError_t e = hipEventRecord(rec.start, stream);
+    if (e != hipSuccess) return e;
+    e = fn();
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(rec.stop, stream);
+    if (e == hipSuccess) g_prof.records.push_back(rec);
+    return e;
+}
+
+rr::RouteArgs route_args(const rr_config &c, const void *Q, const void *K)
+{
+    rr::RouteArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.Q = Q;
+    a.K = K;
+    a.n_heads = c.n_heads;
+    a.n_kv_heads = c.n_kv_heads;
+    a.n_q = c.n_q;
+    a.n_k = c.n_k;
+    a.d = c.d;
+    a.k = c.k;
+    a.m = c.m;
+    a.r = c.r;
+    a.causal = c.causal;
+    a.tiles_per_head = (c.n_q + rr::kTileRows - 1) / rr::kTileRows;
+    a.seed = c.seed;
+    return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *rr_status_string(rr_status s)
+{
+    switch (s) {
+    case RR_OK: return "ok";
+    case RR_ERR_INVALID: return "invalid argument";
+    case RR_ERR_OOM: return "out of device memory";
+    case RR_ERR_HIP: return "HIP runtime error";
+    case RR_ERR_STATE: return "call order violated";
+    case RR_ERR_UNSUPPORTED: return "unsupported configuration";
+    }
+    return "unknown status";
+}
+
+const char *rr_last_error(void) { return g_err.c_str(); }
+
+size_t rr_ledger_index_bytes(const rr_config *c)
+{
+    if (!c) return 0;
+    return (size_t)rows_of(*c) * (size_t)(c->k + c->m + c->r) * sizeof(int32_t);
+}
+
+rr_status rr_ledger_create(const rr_config *cfg, rr_ledger **out)
+{
+    if (!out) return fail(RR_ERR_INVALID, "out is NULL");
+    *out = nullptr;
+    rr_status st = validate(cfg, true);
+    if (st != RR_OK) return st;
+    rr_ledger *L = new (std::nothrow) rr_ledger;
+    if (!L) return fail(RR_ERR_OOM, "host allocation failed");
+    std::memset(L, 0, sizeof(*L));
+    L->cfg = *cfg;
+    L->rows = rows_of(*cfg);
+    L->last_layer = -1;
+    if (hipGetDevice(&L->device) != hipSuccess) {
+        delete L;
+        return fail(RR_ERR_HIP, "hipGetDevice failed");
+    }
+    const int64_t rows = L->rows;
+    const int H = cfg->n_heads;
+    if ((st = alloc(&L->routes, rows * cfg->k, "routes")) != RR_OK ||
+        (st = alloc(&L->sent, rows * (cfg->m + cfg->r), "sentinels")) != RR_OK ||
+        (st = alloc(&L->build, rows, "build")) != RR_OK || (st = alloc(&L->age, rows, "age")) != RR_OK ||
+        (st = alloc(&L->ids, rows, "ids")) != RR_OK || (st = alloc(&L->tile_base, H + 1, "tile_base")) != RR_OK ||
+        (st = alloc(&L->stat_nrr, 1, "stat_nrr")) != RR_OK || (st = alloc(&L->flags, rows, "flags")) != RR_OK ||
+        (st = alloc(&L->alpha, rows, "alpha")) != RR_OK || (st = alloc(&L->beta, rows, "beta")) != RR_OK ||
+        (st = alloc(&L->theta, rows, "theta")) != RR_OK || (st = alloc(&L->acc_pairs, 1, "acc_pairs")) != RR_OK ||
+        (st = alloc(&L->acc_count, H, "acc_count")) != RR_OK || (st = alloc(&L->ticket, 1, "ticket")) != RR_OK ||
+        (st = alloc(&L->stat_pairs, 1, "stat_pairs")) != RR_OK) {
+        free_all(L);
+        delete L;
+        return st;
+    }
+    // One-time initialisation (outside any hot path): the accumulators and
+    // ticket of the rescoring kernel start at zero and are left at zero by it.
+    hipError_t e = hipMemset(L->acc_pairs, 0, sizeof(unsigned long long));
+    if (e == hipSuccess) e = hipMemset(L->acc_count, 0, sizeof(uint32_t) * H);
+    if (e == hipSuccess) e = hipMemset(L->ticket, 0, sizeof(uint32_t));
+    if (e == hipSuccess) e = hipMemset(L->tile_base, 0, sizeof(int32_t) * (H + 1));
+    if (e == hipSuccess) e = hipMemset(L->routes, 0xFF, sizeof(int32_t) * rows * cfg->k);
+    if (e == hipSuccess && cfg->m + cfg->r > 0) e = hipMemset(L->sent, 0xFF, sizeof(int32_t) * rows * (cfg->m + cfg->r));
+    if (e == hipSuccess) e = hipMemset(L->build, 0xFF, sizeof(int32_t) * rows);
+    if (e == hipSuccess) e = hipMemset(L->age, 0, sizeof(int32_t) * rows);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e != hipSuccess) {
+        free_all(L);
+        delete L;
+        return hip_fail(e, "ledger initialisation");
+    }
+    *out = L;
+    return RR_OK;
+}
+
+rr_status rr_ledger_destroy(rr_ledger *L)
+{
+    if (!L) return RR_OK;
+    DeviceGuard g(L->device);
+    (void)hipDeviceSynchronize();
+    free_all(L);
+    delete L;
+    return RR_OK;
+}
+
+rr_status rr_anchor_route(rr_ledger *L, int32_t layer, const void *Qc, const void *Kc, int32_t *routes,
+                          int64_t *pairs, void *hip_stream)
+{
+    if (!L) return fail(RR_ERR_INVALID, "ledger is NULL");
+    if (!Qc || !Kc) return fail(RR_ERR_INVALID, "Qc and Kc must be device pointers");
+    if (layer < 0) return fail(RR_ERR_INVALID, "layer must be >= 0");
+    DeviceGuard g(L->device);
+    const rr_config &c = L->cfg;
+    rr::RouteArgs a = route_args(c, Qc, Kc);
+    a.layer = layer;
+    a.mode = rr::MODE_ANCHOR;
+    a.routes_out = routes;
+    a.led_routes = L->routes;
+    a.led_sent = L->sent;
+    a.led_build = L->build;
+    a.led_age = L->age;
+    a.pairs_out = pairs;
+    a.pairs_value = full_pairs(c);
+    const int grid = c.n_heads * a.tiles_per_head;
+    hipStream_t stream = reinterpret_cast<hipStream_t>(hip_stream);
+    hipError_t e = timed(RR_KERNEL_ANCHOR, stream, [&] { return rr::launch_route(a, c.dtype, grid, stream); });
+    if (e != hipSuccess) return hip_fail(e, "anchor route launch");
+    L->has_state = true;
+    L->last_layer = layer;
+    return RR_OK;
+}
+
+rr_status rr_relay_layer(rr_ledger *L, int32_t layer, const void *Qc, const void *Kc, int32_t *routes,
+                         uint8_t *mask, int64_t *pairs, int32_t *n_rerouted, void *hip_stream)
+{
+    if (!L) return fail(RR_ERR_INVALID, "ledger is NULL");
+    if (!Qc || !Kc) return fail(RR_ERR_INVALID, "Qc and Kc must be device pointers");
+    if (!L->has_state) return fail(RR_ERR_STATE, "relay before any anchor or import");
+    if (layer < L->last_layer) return fail(RR_ERR_STATE, "layer is below the previous call's layer");
+    DeviceGuard g(L->device);
+    const rr_config &c = L->cfg;
+    hipStream_t stream = reinterpret_cast<hipStream_t>(hip_stream);
+
+    rr::RescoreArgs s;
+    std::memset(&s, 0, sizeof(s));
+    s.Q = Qc;
+    s.K = Kc;
+    s.n_heads = c.n_heads;
+    s.n_kv_heads = c.n_kv_heads;
+    s.n_q = c.n_q;
+    s.n_k = c.n_k;
+    s.d = c.d;
+    s.k = c.k;
+    s.m = c.m;
+    s.r = c.r;
+    s.causal = c.causal;
+    s.layer = layer;
+    s.blocks_per_head = (c.n_q + rr::kRescoreRows - 1) / rr::kRescoreRows;
+    s.gamma = c.gamma;
+    s.led_routes = L->routes;
+    s.led_sent = L->sent;
+    s.led_build = L->build;
+    s.led_age = L->age;
+    s.flags = L->flags;
+    s.mask_out = mask;
+    s.alpha = L->alpha;
+    s.beta = L->beta;
+    s.theta = L->theta;
+    s.acc_pairs = L->acc_pairs;
+    s.acc_count = L->acc_count;
+    s.ticket = L->ticket;
+    s.tile_base = L->tile_base;
+    s.stat_pairs = L->stat_pairs;
+    s.stat_nrr = L->stat_nrr;
+    s.pairs_out = pairs;
+    s.nrr_out = n_rerouted;
+    hipError_t e = timed(RR_KERNEL_RESCORE, stream, [&] { return rr::launch_rescore(s, c.dtype, stream); });
+    if (e != hipSuccess) return hip_fail(e, "rescore launch");
+
+    rr::RouteArgs a = route_args(c, Qc, Kc);
+    a.layer = layer;
+    a.mode = rr::MODE_REROUTE;
+    a.led_routes = L->routes;
+    a.led_sent = L->sent;
+    a.led_build = L->build;
+    a.led_age = L->age;
+    a.flags = L->flags;
+    a.theta = L->theta;
+    a.tile_base = L->tile_base;
+    a.ids_out = L->ids;
+    const int max_tiles = c.n_heads * a.tiles_per_head;
+    const int grid = max_tiles < 1024 ? max_tiles : 1024;
+    e = timed(RR_KERNEL_REROUTE, stream, [&] { return rr::launch_route(a, c.dtype, grid, stream); });
+    if (e != hipSuccess) return hip_fail(e, "reroute launch");
+    if (routes) {
+        e = hipMemcpyAsync(routes, L->routes, sizeof(int32_t) * L->rows * c.k, hipMemcpyDeviceToDevice, stream);
+        if (e != hipSuccess) return hip_fail(e, "route copy");
+    }
+    L->last_layer = layer;
+    return RR_OK;
+}
+
+rr_status rr_full_route(const rr_config *cfg, const void *Qc, const void *Kc, int32_t *routes, float *route_scores,
+                        int64_t *pairs, void *hip_stream)
+{
+    rr_status st = validate(cfg, false);
+    if (st != RR_OK) return st;
+    if (!Qc || !Kc || !routes) return fail(RR_ERR_INVALID, "Qc, Kc and routes must be device pointers");
+    rr_config c = *cfg;
+    c.m = 0;
+    c.r = 0;
+    rr::RouteArgs a = route_args(c, Qc, Kc);
+    a.mode = rr::MODE_FULL;
+    a.routes_out = routes;
+    a.scores_out = route_scores;
+    a.pairs_out = pairs;
+    a.pairs_value = full_pairs(c);
+    const int grid = c.n_heads * a.tiles_per_head;
+    hipStream_t stream = reinterpret_cast<hipStream_t>(hip_stream);
+    hipError_t e = timed(RR_KERNEL_FULL, stream, [&] { return rr::launch_route(a, c.dtype, grid, stream); });
+    if (e != hipSuccess) return hip_fail(e, "full route launch");
+    return RR_OK;
+}
+
+const int32_t *rr_ledger_routes(const rr_ledger *L) { return L ? L->routes : nullptr; }
+
+rr_status rr_ledger_export(const rr_ledger *L, int32_t *routes, int32_t *sent, int32_t *build, int32_t *age,
+                           void *hip_stream)
+{
+    if (!L) return fail(RR_ERR_INVALID, "ledger is NULL");
+    DeviceGuard g(L->device);
+    hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+    const rr_config &c = L->cfg;
+    hipError_t e = hipSuccess;
+    if (routes) e = hipMemcpyAsync(routes, L->routes, sizeof(int32_t) * L->rows * c.k, hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess && sent && c.m + c.r > 0)
+        e = hipMemcpyAsync(sent, L->sent, sizeof(int32_t) * L->rows * (c.m + c.r), hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess && build) e = hipMemcpyAsync(build, L->build, sizeof(int32_t) * L->rows, hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess && age) e = hipMemcpyAsync(age, L->age, sizeof(int32_t) * L->rows, hipMemcpyDeviceToDevice, s);
+    return e == hipSuccess ? RR_OK : hip_fail(e, "ledger export");
+}
+
+rr_status rr_ledger_import(rr_ledger *L, int32_t layer, const int32_t *routes, const int32_t *sent,
+                           const int32_t *build, const int32_t *age, void *hip_stream)
+{
+    if (!L) return fail(RR_ERR_INVALID, "ledger is NULL");
+    const rr_config &c = L->cfg;
+    if (!routes || !build || !age || (!sent && c.m + c.r > 0))
+        return fail(RR_ERR_INVALID, "routes, sent, build and age are required");
+    if (layer < 0) return fail(RR_ERR_INVALID, "layer must be >= 0");
+    DeviceGuard g(L->device);
+    hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+    hipError_t e = hipMemcpyAsync(L->routes, routes, sizeof(int32_t) * L->rows * c.k, hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess && c.m + c.r > 0)
+        e = hipMemcpyAsync(L->sent, sent, sizeof(int32_t) * L->rows * (c.m + c.r), hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(L->build, build, sizeof(int32_t) * L->rows, hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(L->age, age, sizeof(int32_t) * L->rows, hipMemcpyDeviceToDevice, s);
+    if (e != hipSuccess) return hip_fail(e, "ledger import");
+    L->has_state = true;
+    L->last_layer = layer;
+    return RR_OK;
+}
+
+rr_status rr_ledger_relay_stats(const rr_ledger *L, float *alpha, float *beta, int32_t *ids, void *hip_stream)
+{
+    if (!L) return fail(RR_ERR_INVALID, "ledger is NULL");
+    DeviceGuard g(L->device);
+    hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+    hipError_t e = hipSuccess;
+    if (alpha) e = hipMemcpyAsync(alpha, L->alpha, sizeof(float) * L->rows, hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess && beta) e = hipMemcpyAsync(beta, L->beta, sizeof(float) * L->rows, hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess && ids) e = hipMemcpyAsync(ids, L->ids, sizeof(int32_t) * L->rows, hipMemcpyDeviceToDevice, s);
+    return e == hipSuccess ? RR_OK : hip_fail(e, "relay stats copy");
+}
+
+rr_status rr_profile_start(void)
+{
+    for (ProfRecord &r : g_prof.records) {
+        g_prof.pool.push_back(r.start);
+        g_prof.pool.push_back(r.stop);
+    }
+    g_prof.records.clear();
+    g_prof.on = true;
+    return RR_OK;
+}
+
+rr_status rr_profile_stop(double *total_ms, int64_t *launches)
+{
+    g_prof.on = false;
+    double ms[RR_KERNEL_KINDS] = {0, 0, 0, 0};
+    int64_t n[RR_KERNEL_KINDS] = {0, 0, 0, 0};
+    rr_status st = RR_OK;
+    for (ProfRecord &r : g_prof.records) {
+        hipError_t e = hipEventSynchronize(r.stop);
+        float t = 0.f;
+        if (e == hipSuccess) e = hipEventElapsedTime(&t, r.start, r.stop);
+        if (e != hipSuccess) {
+            st = hip_fail(e, "profile event");
+            continue;
+        }
+        ms[r.kind] += t;
+        n[r.kind] += 1;
+    }
+    for (int k = 0; k < RR_KERNEL_KINDS; ++k) {
+        if (total_ms) total_ms[k] = ms[k];
+        if (launches) launches[k] = n[k];
+    }
+    return st;
+}
+
+}  // extern "C"

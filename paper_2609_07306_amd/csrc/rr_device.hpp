@@ -1,0 +1,156 @@
+// Device helpers of the gfx950 route-maintenance kernels: operand fragments
+// for the 32x32 MFMA tiles, the total rank order of (score, chunk id), wave
+// shuffles and the random-probe counter hash.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rr {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+// Storage tag of bf16 inputs (the bits are read as __bf16 vectors).
+struct bf16_t {
+    uint16_t bits;
+};
+
+// ---------------------------------------------------------------- ordering
+//
+// Rank order: a higher score ranks first; equal scores rank the lower chunk
+// id first; -0 and +0 are the same score.  rank_key maps (score, id) to a
+// 64-bit integer that is larger exactly when the pair ranks earlier, so all
+// keys of a row are distinct.
+
+__device__ __forceinline__ uint32_t float_order(float s)
+{
+    uint32_t b = __float_as_uint(s);
+    if (b == 0x80000000u) b = 0u;
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+__device__ __forceinline__ float order_float(uint32_t o)
+{
+    uint32_t b = (o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o;
+    return __uint_as_float(b);
+}
+
+__device__ __forceinline__ uint64_t rank_key(float s, int32_t id)
+{
+    return ((uint64_t)float_order(s) << 32) | (uint64_t)(uint32_t)(~id);
+}
+
+__device__ __forceinline__ int32_t key_id(uint64_t key) { return (int32_t)(~(uint32_t)key); }
+
+__device__ __forceinline__ float key_score(uint64_t key) { return order_float((uint32_t)(key >> 32)); }
+
+// ---------------------------------------------------------------- shuffles
+
+__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src)
+{
+    uint32_t lo = (uint32_t)__shfl((int)(uint32_t)v, src, 64);
+    uint32_t hi = (uint32_t)__shfl((int)(uint32_t)(v >> 32), src, 64);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int mask)
+{
+    uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, mask, 64);
+    uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), mask, 64);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint32_t lanemask_lt32(int l32) { return (1u << l32) - 1u; }
+
+// ------------------------------------------------------------ probe hash
+//
+// splitmix64 output function (Steele, Lea and Flood, OOPSLA 2014): add the
+// golden-ratio increment, two xor-shift-multiply rounds, a final xor-shift.
+// A random-sentinel probe hashes (seed, layer, row, slot, attempt) by mixing
+// each coordinate in with xor and applying the function again.
+
+__device__ __forceinline__ uint64_t sm64(uint64_t z)
+{
+    z += 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+// --------------------------------------------------------------- fragments
+//
+// One lane of a 32x32 MFMA holds, for its row (A) or column (B) lane%32, the
+// contiguous half [hh*D/2, (hh+1)*D/2) of the d-dimension, hh = lane/32.  A
+// and B use the same split, so every product pairs equal d-indices and the
+// sum over the whole d-range is the score.
+
+template <typename DT, int D>
+struct Frag;
+
+template <int D>
+struct Frag<float, D> {
+    static constexpr int NS = D / 2;  // v_mfma_f32_32x32x2_f32 steps
+    float v[NS];
+
+    __device__ __forceinline__ void load(const float *row, int hh)
+    {
+        const float4 *p = reinterpret_cast<const float4 *>(row + hh * (D / 2));
+#pragma unroll
+        for (int j = 0; j < D / 8; ++j) {
+            float4 x = p[j];
+            v[4 * j + 0] = x.x;
+            v[4 * j + 1] = x.y;
+            v[4 * j + 2] = x.z;
+            v[4 * j + 3] = x.w;
+        }
+    }
+
+    __device__ __forceinline__ void zero()
+    {
+#pragma unroll
+        for (int s = 0; s < NS; ++s) v[s] = 0.f;
+    }
+
+    __device__ __forceinline__ static f32x16_t mma(const Frag &a, const Frag &b, f32x16_t c)
+    {
+#pragma unroll
+        for (int s = 0; s < NS; ++s) c = __builtin_amdgcn_mfma_f32_32x32x2f32(a.v[s], b.v[s], c, 0, 0, 0);
+        return c;
+    }
+};
+
+template <int D>
+struct Frag<bf16_t, D> {
+    static constexpr int NS = D / 16;  // v_mfma_f32_32x32x16_bf16 steps
+    bf16x8_t v[NS];
+
+    __device__ __forceinline__ void load(const bf16_t *row, int hh)
+    {
+        const bf16x8_t *p = reinterpret_cast<const bf16x8_t *>(row + hh * (D / 2));
+#pragma unroll
+        for (int j = 0; j < NS; ++j) v[j] = p[j];
+    }
+
+    __device__ __forceinline__ void zero()
+    {
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[s][e] = (__bf16)0.0f;
+        }
+    }
+
+    __device__ __forceinline__ static f32x16_t mma(const Frag &a, const Frag &b, f32x16_t c)
+    {
+#pragma unroll
+        for (int s = 0; s < NS; ++s) c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.v[s], b.v[s], c, 0, 0, 0);
+        return c;
+    }
+};
+
+// Row of the 32x32 accumulator held in register i by a lane of half hh.
+__device__ __forceinline__ int acc_row(int i, int hh) { return 8 * (i >> 2) + 4 * hh + (i & 3); }
+
+}  // namespace rr

@@ -1,0 +1,75 @@
+// Kernel argument blocks and launchers shared by the host API and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rr {
+
+enum RouteMode : int32_t {
+    MODE_FULL = 0,     // stateless routing, k slots, no sentinels
+    MODE_ANCHOR = 1,   // every row: route + near-miss + random sentinels -> ledger
+    MODE_REROUTE = 2,  // flagged rows only (compacted per head) -> ledger
+};
+
+constexpr int kTileRows = 32;     // query rows per route tile
+constexpr int kRescoreRows = 64;  // rows per rescoring workgroup
+
+struct RouteArgs {
+    const void *Q;
+    const void *K;
+    int32_t n_heads, n_kv_heads, n_q, n_k, d;
+    int32_t k, m, r;  // the kernel selects T = k + m chunks per row
+    int32_t causal;
+    int32_t layer;
+    int32_t mode;
+    int32_t tiles_per_head;  // ceil(n_q / kTileRows)
+    uint64_t seed;
+    int32_t *routes_out;  // [rows, k] or null
+    float *scores_out;    // [rows, k] or null
+    int32_t *led_routes;  // ledger (anchor / reroute)
+    int32_t *led_sent;
+    int32_t *led_build;
+    int32_t *led_age;
+    const uint8_t *flags;      // reroute: [rows]
+    const float *theta;        // reroute: per-row lower bound of the T-th score
+    const int32_t *tile_base;  // reroute: [n_heads + 1] tile offsets per head
+    int32_t *ids_out;          // reroute: compacted row ids per head, or null
+    int64_t *pairs_out;        // optional device scalar
+    int64_t pairs_value;       // value written to pairs_out (full / anchor)
+};
+
+struct RescoreArgs {
+    const void *Q;
+    const void *K;
+    int32_t n_heads, n_kv_heads, n_q, n_k, d;
+    int32_t k, m, r;
+    int32_t causal;
+    int32_t layer;
+    int32_t blocks_per_head;  // ceil(n_q / kRescoreRows)
+    float gamma;
+    const int32_t *led_routes;
+    const int32_t *led_sent;
+    const int32_t *led_build;
+    int32_t *led_age;
+    uint8_t *flags;     // [rows] internal reroute flags
+    uint8_t *mask_out;  // [rows] caller mask or null
+    float *alpha;
+    float *beta;
+    float *theta;
+    unsigned long long *acc_pairs;  // zero between calls
+    uint32_t *acc_count;            // [n_heads], zero between calls
+    uint32_t *ticket;               // zero between calls
+    int32_t *tile_base;             // [n_heads + 1] written by the last block
+    int64_t *stat_pairs;
+    int32_t *stat_nrr;
+    int64_t *pairs_out;  // optional
+    int32_t *nrr_out;    // optional
+};
+
+// Supported (dtype, d) combinations; dtype 0 = binary32, 1 = bf16.
+bool route_supported(int dtype, int d, int T);
+hipError_t launch_route(const RouteArgs &a, int dtype, int grid, hipStream_t stream);
+hipError_t launch_rescore(const RescoreArgs &a, int dtype, hipStream_t stream);
+
+}  // namespace rr

@@ -1,0 +1,255 @@
+"""ctypes binding of librouterelay.so (C ABI in include/routerelay.h).
+
+Argument marshalling only: every step of the path runs in the library's HIP
+kernels.  Tensors are torch device tensors that supply ``data_ptr()``; the
+stream is torch's current stream unless one is given.  Importing this module
+loads the library and raises ImportError if it has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "librouterelay.so")
+
+RR_OK, RR_ERR_INVALID, RR_ERR_OOM, RR_ERR_HIP, RR_ERR_STATE, RR_ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
+RR_F32, RR_BF16 = 0, 1
+
+EXPORTED = (
+    "rr_ledger_create", "rr_ledger_destroy", "rr_anchor_route", "rr_relay_layer", "rr_full_route",
+    "rr_ledger_routes", "rr_ledger_export", "rr_ledger_import", "rr_ledger_relay_stats",
+    "rr_ledger_index_bytes", "rr_status_string", "rr_last_error", "rr_profile_start",
+    "rr_profile_stop",
+)
+KERNEL_KINDS = ("full", "anchor", "reroute", "rescore")
+
+
+class RRError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{msg} (status {status})")
+        self.status = status
+
+
+class _Config(ctypes.Structure):
+    _fields_ = [
+        ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("n_q", ctypes.c_int32),
+        ("n_k", ctypes.c_int32), ("d", ctypes.c_int32), ("k", ctypes.c_int32), ("m", ctypes.c_int32),
+        ("r", ctypes.c_int32), ("dtype", ctypes.c_int32), ("causal", ctypes.c_int32),
+        ("gamma", ctypes.c_float), ("reserved", ctypes.c_uint32), ("seed", ctypes.c_uint64),
+    ]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built: run `python -m paper_2609_07306_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i32, cfgp = ctypes.c_void_p, ctypes.c_int32, ctypes.POINTER(_Config)
+    sig = {
+        "rr_ledger_create": (ctypes.c_int, [cfgp, ctypes.POINTER(vp)]),
+        "rr_ledger_destroy": (ctypes.c_int, [vp]),
+        "rr_anchor_route": (ctypes.c_int, [vp, i32, vp, vp, vp, vp, vp]),
+        "rr_relay_layer": (ctypes.c_int, [vp, i32, vp, vp, vp, vp, vp, vp, vp]),
+        "rr_full_route": (ctypes.c_int, [cfgp, vp, vp, vp, vp, vp, vp]),
+        "rr_ledger_routes": (vp, [vp]),
+        "rr_ledger_export": (ctypes.c_int, [vp, vp, vp, vp, vp, vp]),
+        "rr_ledger_import": (ctypes.c_int, [vp, i32, vp, vp, vp, vp, vp]),
+        "rr_ledger_relay_stats": (ctypes.c_int, [vp, vp, vp, vp, vp]),
+        "rr_ledger_index_bytes": (ctypes.c_size_t, [cfgp]),
+        "rr_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "rr_last_error": (ctypes.c_char_p, []),
+        "rr_profile_start": (ctypes.c_int, []),
+        "rr_profile_stop": (ctypes.c_int, [vp, vp]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    return lib
+
+
+lib = _load()
+
+
+def _check(status: int):
+    if status != RR_OK:
+        raise RRError(status, lib.rr_last_error().decode())
+
+
+@dataclass(frozen=True)
+class Config:
+    """Shape and rule parameters (rr_config)."""
+    n_heads: int
+    n_kv_heads: int
+    n_q: int
+    n_k: int
+    d: int
+    k: int
+    m: int = 0
+    r: int = 0
+    dtype: str = "f32"  # "f32" | "bf16"
+    causal: bool = False
+    gamma: float = 0.0
+    seed: int = 0
+
+    @property
+    def rows(self) -> int:
+        return self.n_heads * self.n_q
+
+    def c(self) -> _Config:
+        return _Config(self.n_heads, self.n_kv_heads, self.n_q, self.n_k, self.d, self.k, self.m,
+                       self.r, RR_BF16 if self.dtype == "bf16" else RR_F32, int(self.causal),
+                       float(self.gamma), 0, int(self.seed) & 0xFFFFFFFFFFFFFFFF)
+
+    @staticmethod
+    def of(w) -> "Config":
+        """From a synth.Workload."""
+        return Config(w.n_heads, w.n_kv_heads, w.n, w.n, w.d, w.k, w.m, w.r, w.dtype, w.causal,
+                      w.gamma, w.seed)
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensor must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _inputs(cfg: Config, Q, K):
+    want = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    if Q.dtype != want or K.dtype != want:
+        raise TypeError(f"Qc/Kc must be {want}")
+    if tuple(Q.shape) != (cfg.n_heads, cfg.n_q, cfg.d) or tuple(K.shape) != (cfg.n_kv_heads, cfg.n_k, cfg.d):
+        raise ValueError(f"shapes {tuple(Q.shape)}, {tuple(K.shape)} do not match the config")
+    return _ptr(Q), _ptr(K)
+
+
+def _out(t, shape, dtype):
+    if t is None:
+        return None
+    if tuple(t.shape) != tuple(shape) or t.dtype != dtype:
+        raise ValueError(f"output must be {dtype} of shape {shape}")
+    return _ptr(t)
+
+
+def profile_start():
+    """Start bracketing every library kernel launch with HIP events."""
+    _check(lib.rr_profile_start())
+
+
+def profile_stop():
+    """Stop profiling; returns {kind: (total_ms, launches)}."""
+    ms = (ctypes.c_double * 4)()
+    n = (ctypes.c_int64 * 4)()
+    _check(lib.rr_profile_stop(ms, n))
+    return {k: (ms[i], n[i]) for i, k in enumerate(KERNEL_KINDS)}
+
+
+def index_bytes(cfg: Config) -> int:
+    return int(lib.rr_ledger_index_bytes(ctypes.byref(cfg.c())))
+
+
+def full_route(cfg: Config, Q, K, routes, scores=None, pairs=None, stream=None):
+    """rr_full_route: every row's top-k (Eq. (1)-(2)) into ``routes`` [rows, k] int32."""
+    q, k = _inputs(cfg, Q, K)
+    _check(lib.rr_full_route(ctypes.byref(cfg.c()), q, k, _out(routes, (cfg.rows, cfg.k), torch.int32),
+                             _out(scores, (cfg.rows, cfg.k), torch.float32),
+                             _out(pairs, (1,), torch.int64), _stream(stream)))
+
+
+class Ledger:
+    """rr_ledger: the per-row route ledger on the current device."""
+
+    def __init__(self, cfg: Config):
+        self.cfg = cfg
+        h = ctypes.c_void_p()
+        _check(lib.rr_ledger_create(ctypes.byref(cfg.c()), ctypes.byref(h)))
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None) and self._h.value:
+            lib.rr_ledger_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    @property
+    def handle(self):
+        return self._h
+
+    def anchor(self, layer: int, Q, K, routes=None, pairs=None, stream=None):
+        q, k = _inputs(self.cfg, Q, K)
+        c = self.cfg
+        _check(lib.rr_anchor_route(self._h, layer, q, k, _out(routes, (c.rows, c.k), torch.int32),
+                                   _out(pairs, (1,), torch.int64), _stream(stream)))
+
+    def relay(self, layer: int, Q, K, routes=None, mask=None, pairs=None, n_rerouted=None, stream=None):
+        q, k = _inputs(self.cfg, Q, K)
+        c = self.cfg
+        _check(lib.rr_relay_layer(self._h, layer, q, k, _out(routes, (c.rows, c.k), torch.int32),
+                                  _out(mask, (c.rows,), torch.uint8), _out(pairs, (1,), torch.int64),
+                                  _out(n_rerouted, (1,), torch.int32), _stream(stream)))
+
+    def routes_ptr(self) -> int:
+        return int(lib.rr_ledger_routes(self._h) or 0)
+
+    def export(self, stream=None):
+        """Copies of the ledger state: dict of int32 device tensors."""
+        c = self.cfg
+        dev = torch.device("cuda", torch.cuda.current_device())
+        out = {
+            "routes": torch.empty((c.rows, c.k), dtype=torch.int32, device=dev),
+            "sent": torch.empty((c.rows, c.m + c.r), dtype=torch.int32, device=dev),
+            "build": torch.empty((c.rows,), dtype=torch.int32, device=dev),
+            "age": torch.empty((c.rows,), dtype=torch.int32, device=dev),
+        }
+        _check(lib.rr_ledger_export(self._h, _ptr(out["routes"]), _ptr(out["sent"]) if c.m + c.r else None,
+                                    _ptr(out["build"]), _ptr(out["age"]), _stream(stream)))
+        return out
+
+    def import_(self, layer: int, routes, sent, build, age, stream=None):
+        c = self.cfg
+        _check(lib.rr_ledger_import(self._h, layer, _out(routes, (c.rows, c.k), torch.int32),
+                                    _out(sent, (c.rows, c.m + c.r), torch.int32) if c.m + c.r else None,
+                                    _out(build, (c.rows,), torch.int32), _out(age, (c.rows,), torch.int32),
+                                    _stream(stream)))
+
+    def relay_stats(self, stream=None):
+        c = self.cfg
+        dev = torch.device("cuda", torch.cuda.current_device())
+        alpha = torch.empty(c.rows, dtype=torch.float32, device=dev)
+        beta = torch.empty(c.rows, dtype=torch.float32, device=dev)
+        ids = torch.empty(c.rows, dtype=torch.int32, device=dev)
+        _check(lib.rr_ledger_relay_stats(self._h, _ptr(alpha), _ptr(beta), _ptr(ids), _stream(stream)))
+        return alpha, beta, ids
+
+
+def to_device(x_dev, dtype: str, device="cuda"):
+    """numpy array from synth (binary32 values or bf16 bits) -> torch device tensor."""
+    import numpy as np
+    if dtype == "bf16":
+        t = torch.from_numpy(np.ascontiguousarray(x_dev).view(np.int16)).view(torch.bfloat16)
+    else:
+        t = torch.from_numpy(np.ascontiguousarray(x_dev, dtype=np.float32))
+    return t.to(device)

@@ -1,0 +1,278 @@
+"""GPU parity of the HIP path with the oracle, through the C ABI.
+
+Routes, near-miss and random sentinels, masks, ages and score-pair counts are
+compared bit-exactly on every row whose outcome does not hinge on a near-tie
+(see parity_util); scores within 1e-5 (binary32 inputs) or 2e-3 (bf16 inputs)
+of the oracle relative to sum_t |q_t k_t|.
+"""
+import math
+import sys
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_07306_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    torch.cuda.set_device(0)
+    yield
+
+
+def rrmod():
+    from paper_2609_07306_amd import routerelay
+    return routerelay
+
+
+def note(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+# ------------------------------------------------------------ full routing
+
+FULL_CASES = [
+    # name, H, Hkv, n_q, n_k, d, dtype, k, causal
+    ("tiny_f32", 1, 1, 128, 128, 64, "f32", 8, False),
+    ("ragged_f32", 3, 1, 100, 77, 32, "f32", 5, False),
+    ("ragged_causal", 2, 2, 70, 70, 64, "f32", 9, True),
+    ("drift_f32", 2, 2, 256, 256, 128, "f32", 16, False),
+    ("bf16_d128", 4, 2, 160, 300, 128, "bf16", 32, False),
+    ("bf16_causal_gqa", 4, 1, 200, 200, 128, "bf16", 32, True),
+    ("bf16_d256", 2, 2, 64, 96, 256, "bf16", 12, False),
+    ("bf16_d32_k_eq_nk", 1, 1, 40, 20, 32, "bf16", 20, False),
+    ("wide_k", 2, 2, 64, 512, 128, "bf16", 100, False),
+]
+
+
+def _inputs(rng, H, Hkv, n_q, n_k, d, dtype):
+    Q = (rng.standard_normal((H, n_q, d)) / np.sqrt(d)).astype(np.float32)
+    K = (rng.standard_normal((Hkv, n_k, d)) / np.sqrt(d)).astype(np.float32)
+    if dtype == "bf16":
+        Qd, Kd = synth.bf16_round(Q), synth.bf16_round(K)
+        return synth.bf16_widen(Qd), synth.bf16_widen(Kd), Qd, Kd
+    return Q, K, Q, K
+
+
+@pytest.mark.parametrize("case", FULL_CASES, ids=[c[0] for c in FULL_CASES])
+def test_full_route_parity(case):
+    from parity_util import dev, route_ties, TOL
+    rr = rrmod()
+    name, H, Hkv, n_q, n_k, d, dtype, k, causal = case
+    note(f"full route parity: {case}")
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    Qf, Kf, Qd, Kd = _inputs(rng, H, Hkv, n_q, n_k, d, dtype)
+    cfg = rr.Config(H, Hkv, n_q, n_k, d, k, 0, 0, dtype, causal)
+    p = oracle.Problem(H, Hkv, n_q, n_k, d, k, 0, 0, causal)
+    routes = torch.full((cfg.rows, k), -7, dtype=torch.int32, device="cuda")
+    scores = torch.zeros((cfg.rows, k), dtype=torch.float32, device="cuda")
+    pairs = torch.zeros(1, dtype=torch.int64, device="cuda")
+    rr.full_route(cfg, dev(Qd, dtype), dev(Kd, dtype), routes, scores, pairs)
+    torch.cuda.synchronize()
+    exact, opairs, osc = oracle.full_route(p, Qf, Kf, with_scores=True)
+    t1, _ = route_ties(p, Qf, Kf)
+    got = routes.cpu().numpy()
+    assert int(pairs.item()) == opairs
+    assert t1.mean() < 0.05
+    bad = np.flatnonzero((got != exact).any(1) & ~t1)
+    assert len(bad) == 0, f"rows {bad[:8]}: {got[bad[:2]]} vs {exact[bad[:2]]}"
+    # scores of agreeing rows, relative to sum_t |q_t k_t|
+    sc = scores.cpu().numpy()
+    ok = ~t1
+    valid = exact >= 0
+    for row in np.flatnonzero(ok)[:400]:
+        h, i = divmod(row, n_q)
+        g = h // (H // Hkv)
+        ids = exact[row][valid[row]]
+        absd = np.abs(Qf[h, i].astype(np.float64)[None, :] * Kf[g, ids].astype(np.float64)).sum(1)
+        assert np.all(np.abs(sc[row][valid[row]] - osc[row][valid[row]]) <= TOL[dtype] * absd)
+        assert np.all(np.isneginf(sc[row][~valid[row]]))
+
+
+def test_full_route_exact_ties_integer_data():
+    """Small-integer inputs make every score exact in binary32, so the GPU and
+    the oracle see identical scores with massive exact ties: every row must
+    match, exercising the lower-id tie-break and the overflow repair."""
+    from parity_util import dev
+    rr = rrmod()
+    rng = np.random.default_rng(5)
+    for dtype in ("f32", "bf16"):
+        for causal in (False, True):
+            H, n, d, k = 2, 300, 32, 24
+            Q = rng.integers(-2, 3, size=(H, n, d)).astype(np.float32)
+            K = rng.integers(-1, 2, size=(H, n, d)).astype(np.float32)
+            note(f"integer ties: {dtype} causal={causal}")
+            Qd = synth.bf16_round(Q) if dtype == "bf16" else Q
+            Kd = synth.bf16_round(K) if dtype == "bf16" else K
+            cfg = rr.Config(H, H, n, n, d, k, 0, 0, dtype, causal)
+            routes = torch.empty((cfg.rows, k), dtype=torch.int32, device="cuda")
+            rr.full_route(cfg, dev(Qd, dtype), dev(Kd, dtype), routes)
+            torch.cuda.synchronize()
+            exact, _ = oracle.full_route(oracle.Problem(H, H, n, n, d, k, causal=causal), Q, K)
+            np.testing.assert_array_equal(routes.cpu().numpy(), exact)
+
+
+def test_all_zero_scores_pick_lowest_ids():
+    from parity_util import dev
+    rr = rrmod()
+    H, n, d, k, m, r = 1, 200, 64, 10, 5, 5
+    Q = np.zeros((H, n, d), np.float32)
+    K = np.random.default_rng(1).standard_normal((H, n, d)).astype(np.float32)
+    cfg = rr.Config(H, H, n, n, d, k, m, r, "f32", False)
+    L = rr.Ledger(cfg)
+    L.anchor(0, dev(Q, "f32"), dev(K, "f32"))
+    from parity_util import ledger_np
+    got = ledger_np(L)
+    ref = oracle.new_ledger(oracle.Problem(H, H, n, n, d, k, m, r))
+    oracle.anchor(oracle.Problem(H, H, n, n, d, k, m, r), 0, Q, K, ref)
+    assert (got["routes"] == np.arange(k)).all()
+    for key in ("routes", "sent", "build", "age"):
+        np.testing.assert_array_equal(got[key], ref[key])
+    L.close()
+
+
+# ------------------------------------------------------- rollout parity
+
+ROLLOUTS = [
+    ("tiny", {}),
+    ("tiny", {"causal": True, "n_layers": 6, "anchor_every": 4}),
+    ("drift", {"rho": 0.1}),
+    ("drift", {"rho": 0.3}),
+    ("drift", {"rho": 0.6}),
+    ("scale", {"n_heads": 4, "n_kv_heads": 4, "n": 256, "n_layers": 10}),
+    ("gqa", {"n_heads": 8, "n_kv_heads": 2, "n": 256, "n_layers": 10}),
+    ("longctx", {"n_heads": 2, "n_kv_heads": 2, "n": 512, "n_layers": 10}),
+    ("tiny", {"n": 100, "d": 32, "k": 5, "m": 3, "r": 2, "n_heads": 4, "n_kv_heads": 2, "n_layers": 5}),
+    ("tiny", {"n": 100, "d": 32, "k": 5, "m": 3, "r": 2, "n_heads": 4, "n_kv_heads": 2, "n_layers": 5,
+              "causal": True, "dtype": "bf16"}),
+    ("tiny", {"m": 0, "r": 6, "n_layers": 4}),
+    ("tiny", {"m": 6, "r": 0, "n_layers": 4}),
+]
+
+
+@pytest.mark.parametrize("name,kw", ROLLOUTS, ids=[f"{n}-{i}" for i, (n, _) in enumerate(ROLLOUTS)])
+def test_rollout_parity(name, kw):
+    from parity_util import rollout_compare
+    w = synth.preset(name, **kw)
+    note(f"rollout parity: {name} {kw}")
+    st = rollout_compare(w)
+    note(f"  {st}")
+    assert st["compared"] >= 0.8 * st["rows"]
+
+
+@pytest.mark.parametrize("gamma", [math.inf, -math.inf, 0.05])
+def test_forced_paths(gamma):
+    """gamma = +inf refreshes every row (the relay equals full routing);
+    gamma = -inf refreshes none (the reroute kernel finds no tiles)."""
+    from parity_util import rollout_compare, dev, ledger_np
+    rr = rrmod()
+    w = synth.preset("drift", n_heads=2, n_kv_heads=2, n_layers=4, rho=0.6)
+    note(f"forced path gamma={gamma}")
+    rollout_compare(w, gamma=gamma)
+    if math.isinf(gamma):
+        w2 = w.with_(gamma=gamma)
+        cfg = rr.Config.of(w2)
+        L = rr.Ledger(cfg)
+        lay = synth.layers(w2)
+        L.anchor(0, dev(lay[0][2], w.dtype), dev(lay[0][3], w.dtype))
+        before = ledger_np(L)
+        mask = torch.empty(cfg.rows, dtype=torch.uint8, device="cuda")
+        nrr = torch.zeros(1, dtype=torch.int32, device="cuda")
+        Q1, K1 = dev(lay[1][2], w.dtype), dev(lay[1][3], w.dtype)
+        L.relay(1, Q1, K1, mask=mask, n_rerouted=nrr)
+        after = ledger_np(L)
+        if gamma < 0:
+            assert int(nrr.item()) == 0 and int(mask.sum().item()) == 0
+            for key in ("routes", "sent", "build"):
+                np.testing.assert_array_equal(after[key], before[key])
+        else:
+            assert int(nrr.item()) == cfg.rows
+            full = torch.empty((cfg.rows, cfg.k), dtype=torch.int32, device="cuda")
+            rr.full_route(cfg, Q1, K1, full)
+            torch.cuda.synchronize()
+            np.testing.assert_array_equal(after["routes"], full.cpu().numpy())
+        L.close()
+
+
+# ------------------------------------------- full-size sampled parity
+
+FULL_SIZE = [
+    ("scale", {}),
+    ("scale", {"n": 128}),
+    ("gqa", {}),
+    ("drift", {"rho": 0.3}),
+    ("longctx", {}),
+]
+
+
+@pytest.mark.parametrize("name,kw", FULL_SIZE, ids=[f"{n}-{kw.get('n', '')}" for n, kw in FULL_SIZE])
+def test_full_size_sampled(name, kw):
+    """At the workload's real size, in the launch configuration the benchmark
+    uses: an anchor, then a relay in step mode, checked on sampled rows."""
+    from parity_util import dev, ledger_np, problem_of, route_ties, trigger_ties
+    rr = rrmod()
+    w = synth.preset(name, n_layers=2, **kw)
+    note(f"full-size sampled: {w.name} n={w.n} heads={w.n_heads}")
+    p = problem_of(w)
+    cfg = rr.Config.of(w)
+    gen = list(synth.Generator(w))
+    rng = np.random.default_rng(0)
+    rows = np.unique(np.concatenate([rng.choice(p.rows, 192, replace=False),
+                                     [0, p.rows - 1, p.n_q - 1, p.n_q]]))
+    L = rr.Ledger(cfg)
+    _, Q0f, K0f, Q0d, K0d = gen[0]
+    L.anchor(0, dev(Q0d, w.dtype), dev(K0d, w.dtype))
+    got0 = ledger_np(L)
+    ref = oracle.new_ledger(p)
+    oracle.anchor(p, 0, Q0f, K0f, ref, rows=rows)
+    t1, t2 = route_ties(p, Q0f, K0f, rows=rows)
+    ok = rows[~(t1 | t2)]
+    for key in ("routes", "sent", "build", "age"):
+        np.testing.assert_array_equal(got0[key][ok], ref[key][ok])
+    # step mode: the oracle relays the sampled rows from the GPU's ledger
+    _, Q1f, K1f, Q1d, K1d = gen[1]
+    mask = torch.empty(cfg.rows, dtype=torch.uint8, device="cuda")
+    pairs = torch.zeros(1, dtype=torch.int64, device="cuda")
+    L.relay(1, dev(Q1d, w.dtype), dev(K1d, w.dtype), mask=mask, pairs=pairs)
+    got1 = ledger_np(L)
+    led = {k: v.copy() for k, v in got0.items()}
+    out = oracle.relay(p, 1, Q1f, K1f, led, rows=rows)
+    gm = mask.cpu().numpy()
+    t3 = trigger_ties(p, out)[rows]
+    t1b, t2b = route_ties(p, Q1f, K1f, rows=rows)
+    om = out["mask"][rows]
+    dec = ~t3
+    assert np.array_equal(gm[rows][dec], om[dec])
+    same = dec & ~(om.astype(bool) & (t1b | t2b))
+    for key in ("routes", "sent", "build", "age"):
+        np.testing.assert_array_equal(got1[key][rows[same]], led[key][rows[same]])
+    cand = (got0["routes"] >= 0).sum(1) + (got0["sent"] >= 0).sum(1)
+    ni = np.minimum(np.arange(p.rows) % p.n_q + 1, p.n_k) if p.causal else np.full(p.rows, p.n_k)
+    assert int(pairs.item()) == int(cand.sum() + ni[gm.astype(bool)].sum())
+    note(f"  sampled {len(rows)} rows, rerouted fraction {gm.mean():.3f}")
+    L.close()
+
+
+def test_state_errors():
+    from parity_util import dev
+    rr = rrmod()
+    cfg = rr.Config(1, 1, 64, 64, 64, 4, 2, 2)
+    Q = dev(np.zeros((1, 64, 64), np.float32), "f32")
+    L = rr.Ledger(cfg)
+    with pytest.raises(rr.RRError) as e:
+        L.relay(0, Q, Q)
+    assert e.value.status == rr.RR_ERR_STATE
+    L.anchor(3, Q, Q)
+    with pytest.raises(rr.RRError) as e:
+        L.relay(2, Q, Q)
+    assert e.value.status == rr.RR_ERR_STATE
+    L.relay(3, Q, Q)
+    L.close()
