@@ -16,7 +16,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "librouterelay.so")
-SOURCES = ["rr_api.hip", "rr_route.hip", "rr_rescore.hip"]
+SOURCES = ["rr_api.hip", "rr_route.hip", "rr_rescore.hip", "rr_route_f32_w2.hip", "rr_route_f32_w4.hip",
+           "rr_route_bf16_w2.hip", "rr_route_bf16_w4.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

@@ -169,7 +169,8 @@ rr::RouteArgs route_args(const rr_config &c, const void *Q, const void *K)
     a.m = c.m;
     a.r = c.r;
     a.causal = c.causal;
-    a.tiles_per_head = (c.n_q + rr::kTileRows - 1) / rr::kTileRows;
+    const int tr = rr::route_tile_rows(rr::MODE_FULL);
+    a.tiles_per_head = (c.n_q + tr - 1) / tr;
     a.seed = c.seed;
     return a;
 }
@@ -314,6 +315,7 @@ rr_status rr_relay_layer(rr_ledger *L, int32_t layer, const void *Qc, const void
     s.layer = layer;
     s.blocks_per_head = (c.n_q + rr::kRescoreRows - 1) / rr::kRescoreRows;
     s.gamma = c.gamma;
+    s.reroute_tile_rows = rr::route_tile_rows(rr::MODE_REROUTE);
     s.led_routes = L->routes;
     s.led_sent = L->sent;
     s.led_build = L->build;
@@ -345,7 +347,8 @@ rr_status rr_relay_layer(rr_ledger *L, int32_t layer, const void *Qc, const void
     a.theta = L->theta;
     a.tile_base = L->tile_base;
     a.ids_out = L->ids;
-    const int max_tiles = c.n_heads * a.tiles_per_head;
+    const int rt = rr::route_tile_rows(rr::MODE_REROUTE);
+    const int max_tiles = c.n_heads * ((c.n_q + rt - 1) / rt);
     const int grid = max_tiles < 1024 ? max_tiles : 1024;
     e = timed(RR_KERNEL_REROUTE, stream, [&] { return rr::launch_route(a, c.dtype, grid, stream); });
     if (e != hipSuccess) return hip_fail(e, "reroute launch");

@@ -150,6 +150,25 @@ struct Frag<bf16_t, D> {
     }
 };
 
+// Workgroup-to-(head, tile) map.  With a multiple of 8 key heads, the tiles
+// of key head g go to workgroups b with b % 8 == g % 8: workgroups are handed
+// to the 8 XCDs round-robin, so each XCD's L2 serves the key rows of its own
+// heads only.
+__device__ __forceinline__ void tile_of_block(int b, int H, int Hkv, int tph, int &h, int &t)
+{
+    const int group = H / Hkv;
+    if ((Hkv & 7) == 0) {
+        const int x = b & 7, local = b >> 3;
+        const int j = local / tph;
+        t = local - j * tph;
+        const int g = x + 8 * (j / group);
+        h = g * group + (j - (j / group) * group);
+    } else {
+        h = b / tph;
+        t = b - h * tph;
+    }
+}
+
 // Row of the 32x32 accumulator held in register i by a lane of half hh.
 __device__ __forceinline__ int acc_row(int i, int hh) { return 8 * (i >> 2) + 4 * hh + (i & 3); }
 

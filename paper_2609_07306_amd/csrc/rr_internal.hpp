@@ -12,8 +12,9 @@ enum RouteMode : int32_t {
     MODE_REROUTE = 2,  // flagged rows only (compacted per head) -> ledger
 };
 
-constexpr int kTileRows = 32;     // query rows per route tile
-constexpr int kRescoreRows = 64;  // rows per rescoring workgroup
+constexpr int kFullWaves = 4;     // waves (x 32 rows) per full / anchor route tile
+constexpr int kRerouteWaves = 2;  // waves (x 32 rows) per reroute tile
+constexpr int kRescoreRows = 32;  // rows per rescoring workgroup (4 waves)
 
 struct RouteArgs {
     const void *Q;
@@ -23,7 +24,8 @@ struct RouteArgs {
     int32_t causal;
     int32_t layer;
     int32_t mode;
-    int32_t tiles_per_head;  // ceil(n_q / kTileRows)
+    int32_t tiles_per_head;  // ceil(n_q / tile rows) for full / anchor tiles
+    int32_t lds_region0;     // set by the launcher: bytes of the key-tile region
     uint64_t seed;
     int32_t *routes_out;  // [rows, k] or null
     float *scores_out;    // [rows, k] or null
@@ -47,6 +49,7 @@ struct RescoreArgs {
     int32_t causal;
     int32_t layer;
     int32_t blocks_per_head;  // ceil(n_q / kRescoreRows)
+    int32_t reroute_tile_rows;
     float gamma;
     const int32_t *led_routes;
     const int32_t *led_sent;
@@ -69,6 +72,7 @@ struct RescoreArgs {
 
 // Supported (dtype, d) combinations; dtype 0 = binary32, 1 = bf16.
 bool route_supported(int dtype, int d, int T);
+int route_tile_rows(int mode);
 hipError_t launch_route(const RouteArgs &a, int dtype, int grid, hipStream_t stream);
 hipError_t launch_rescore(const RescoreArgs &a, int dtype, hipStream_t stream);
 
