@@ -19,7 +19,7 @@ struct rr_ledger {
     int64_t rows;
     int32_t *routes, *sent, *build, *age, *ids, *tile_base, *stat_nrr;
     uint8_t *flags;
-    float *alpha, *beta, *theta;
+    float *alpha, *beta;
     unsigned long long *acc_pairs;
     uint32_t *acc_count, *ticket;
     int64_t *stat_pairs;
@@ -105,7 +105,7 @@ rr_status alloc(T **p, int64_t n, const char *what)
 void free_all(rr_ledger *L)
 {
     void *ptrs[] = {L->routes, L->sent,  L->build, L->age,       L->ids,       L->tile_base,
-                    L->stat_nrr, L->flags, L->alpha, L->beta, L->theta, L->acc_pairs,
+                    L->stat_nrr, L->flags, L->alpha, L->beta, L->acc_pairs,
                     L->acc_count, L->ticket, L->stat_pairs};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);
@@ -169,7 +169,7 @@ rr::RouteArgs route_args(const rr_config &c, const void *Q, const void *K)
     a.m = c.m;
     a.r = c.r;
     a.causal = c.causal;
-    const int tr = rr::route_tile_rows(rr::MODE_FULL);
+    const int tr = rr::route_tile_rows(c.k + c.m);
     a.tiles_per_head = (c.n_q + tr - 1) / tr;
     a.seed = c.seed;
     return a;
@@ -224,7 +224,7 @@ rr_status rr_ledger_create(const rr_config *cfg, rr_ledger **out)
         (st = alloc(&L->ids, rows, "ids")) != RR_OK || (st = alloc(&L->tile_base, H + 1, "tile_base")) != RR_OK ||
         (st = alloc(&L->stat_nrr, 1, "stat_nrr")) != RR_OK || (st = alloc(&L->flags, rows, "flags")) != RR_OK ||
         (st = alloc(&L->alpha, rows, "alpha")) != RR_OK || (st = alloc(&L->beta, rows, "beta")) != RR_OK ||
-        (st = alloc(&L->theta, rows, "theta")) != RR_OK || (st = alloc(&L->acc_pairs, 1, "acc_pairs")) != RR_OK ||
+        (st = alloc(&L->acc_pairs, 1, "acc_pairs")) != RR_OK ||
         (st = alloc(&L->acc_count, H, "acc_count")) != RR_OK || (st = alloc(&L->ticket, 1, "ticket")) != RR_OK ||
         (st = alloc(&L->stat_pairs, 1, "stat_pairs")) != RR_OK) {
         free_all(L);
@@ -315,7 +315,7 @@ rr_status rr_relay_layer(rr_ledger *L, int32_t layer, const void *Qc, const void
     s.layer = layer;
     s.blocks_per_head = (c.n_q + rr::kRescoreRows - 1) / rr::kRescoreRows;
     s.gamma = c.gamma;
-    s.reroute_tile_rows = rr::route_tile_rows(rr::MODE_REROUTE);
+    s.reroute_tile_rows = rr::route_tile_rows(c.k + c.m);
     s.led_routes = L->routes;
     s.led_sent = L->sent;
     s.led_build = L->build;
@@ -324,7 +324,6 @@ rr_status rr_relay_layer(rr_ledger *L, int32_t layer, const void *Qc, const void
     s.mask_out = mask;
     s.alpha = L->alpha;
     s.beta = L->beta;
-    s.theta = L->theta;
     s.acc_pairs = L->acc_pairs;
     s.acc_count = L->acc_count;
     s.ticket = L->ticket;
@@ -344,12 +343,12 @@ rr_status rr_relay_layer(rr_ledger *L, int32_t layer, const void *Qc, const void
     a.led_build = L->build;
     a.led_age = L->age;
     a.flags = L->flags;
-    a.theta = L->theta;
     a.tile_base = L->tile_base;
     a.ids_out = L->ids;
-    const int rt = rr::route_tile_rows(rr::MODE_REROUTE);
+    const int rt = rr::route_tile_rows(c.k + c.m);
     const int max_tiles = c.n_heads * ((c.n_q + rt - 1) / rt);
-    const int grid = max_tiles < 1024 ? max_tiles : 1024;
+    const int grid8 = (max_tiles + 7) & ~7;  // a multiple of 8: per-XCD tile ranges
+    const int grid = grid8 < 1024 ? grid8 : 1024;
     e = timed(RR_KERNEL_REROUTE, stream, [&] { return rr::launch_route(a, c.dtype, grid, stream); });
     if (e != hipSuccess) return hip_fail(e, "reroute launch");
     if (routes) {

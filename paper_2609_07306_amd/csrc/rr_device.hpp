@@ -169,6 +169,18 @@ __device__ __forceinline__ void tile_of_block(int b, int H, int Hkv, int tph, in
     }
 }
 
+// Query head at position j of the XCD-major head order: with a multiple of 8
+// key heads, positions [x*H/8, (x+1)*H/8) hold the query heads whose key head
+// g has g % 8 == x, so per-XCD work lists are contiguous.
+__device__ __forceinline__ int head_at(int j, int H, int Hkv)
+{
+    if ((Hkv & 7) != 0) return j;
+    const int group = H / Hkv, hx = H >> 3;
+    const int x = j / hx, local = j - x * hx;
+    const int g = x + 8 * (local / group);
+    return g * group + (local - (local / group) * group);
+}
+
 // Row of the 32x32 accumulator held in register i by a lane of half hh.
 __device__ __forceinline__ int acc_row(int i, int hh) { return 8 * (i >> 2) + 4 * hh + (i & 3); }
 

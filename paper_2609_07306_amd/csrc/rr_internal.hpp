@@ -12,8 +12,8 @@ enum RouteMode : int32_t {
     MODE_REROUTE = 2,  // flagged rows only (compacted per head) -> ledger
 };
 
-constexpr int kFullWaves = 4;     // waves (x 32 rows) per full / anchor route tile
-constexpr int kRerouteWaves = 2;  // waves (x 32 rows) per reroute tile
+constexpr int kNarrowTileRows = 128;  // route tile rows when k + m <= 64
+constexpr int kWideTileRows = 64;     // route tile rows when 64 < k + m <= 128
 constexpr int kRescoreRows = 32;  // rows per rescoring workgroup (4 waves)
 
 struct RouteArgs {
@@ -34,8 +34,7 @@ struct RouteArgs {
     int32_t *led_build;
     int32_t *led_age;
     const uint8_t *flags;      // reroute: [rows]
-    const float *theta;        // reroute: per-row lower bound of the T-th score
-    const int32_t *tile_base;  // reroute: [n_heads + 1] tile offsets per head
+    const int32_t *tile_base;  // reroute: [n_heads + 1] tile offsets, XCD-major head order
     int32_t *ids_out;          // reroute: compacted row ids per head, or null
     int64_t *pairs_out;        // optional device scalar
     int64_t pairs_value;       // value written to pairs_out (full / anchor)
@@ -59,7 +58,6 @@ struct RescoreArgs {
     uint8_t *mask_out;  // [rows] caller mask or null
     float *alpha;
     float *beta;
-    float *theta;
     unsigned long long *acc_pairs;  // zero between calls
     uint32_t *acc_count;            // [n_heads], zero between calls
     uint32_t *ticket;               // zero between calls
@@ -72,7 +70,7 @@ struct RescoreArgs {
 
 // Supported (dtype, d) combinations; dtype 0 = binary32, 1 = bf16.
 bool route_supported(int dtype, int d, int T);
-int route_tile_rows(int mode);
+int route_tile_rows(int T);  // query rows per route tile for T = k + m
 hipError_t launch_route(const RouteArgs &a, int dtype, int grid, hipStream_t stream);
 hipError_t launch_rescore(const RescoreArgs &a, int dtype, hipStream_t stream);
 

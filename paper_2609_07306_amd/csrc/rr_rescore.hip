@@ -3,25 +3,23 @@
 //
 // Each row's candidates are its ledger slots: R (k slots), then the near-miss
 // sentinels (m) and the random sentinels (r); -1 slots are empty.  A wave
-// works on one row at a time: one coalesced load brings all of the row's
-// slot ids (lane j holds slot j), then the wave scores 16 candidates per
-// round -- 4 lanes share a candidate's key row, each reading 16-byte pieces
-// so that one load instruction covers 64 contiguous bytes of 16 rows -- with
-// the loads of several rounds in flight before any product is formed, and the
-// next row's ids and query already requested.  The 4 partial dots of a
-// candidate are summed with two lane swaps.
-//
-// From the scores it forms alpha = min over R, beta = max over C and the
-// refresh flag (C non-empty and beta + gamma >= alpha).  For a refreshed row
-// it also records theta = the (k+m)-th best candidate score: the row has at
-// least k+m chunks scoring >= theta, so theta bounds its new (k+m)-th score
-// from below and seeds the reroute kernel's threshold.  Rows that keep their
-// route get age = layer - build layer.
+// scores its rows one after another: one coalesced load brings all of a row's
+// slot ids (lane j holds slot j), then 16 candidates per round -- 4 lanes
+// share a candidate's key row, each reading 16-byte pieces so that one load
+// instruction covers 64 contiguous bytes of 16 rows -- with the loads of all
+// rounds in flight before any product is formed and the next row's ids and
+// query already requested.  The 4 partial dots of a candidate are summed with
+// two DPP quad permutations and the score goes to LDS.  A second phase gives
+// each row to one lane, which forms alpha = min over R, beta = max over C and
+// the refresh flag (C non-empty and beta + gamma >= alpha), and sets
+// age = layer - build layer on rows that keep their route.
 //
 // Score-pair counts and per-head refresh counts go to device accumulators;
 // the last workgroup to finish (ticket counter) turns the per-head counts
-// into the reroute kernel's tile table, publishes the totals and zeroes the
-// accumulators and the ticket for the next call.  No host synchronisation.
+// into the reroute kernel's tile table (heads in XCD-major order, so each
+// XCD's reroute workgroups find their tiles in one contiguous range),
+// publishes the totals and zeroes the accumulators and the ticket for the
+// next call.  No host synchronisation.
 #include <math.h>
 
 #include "rr_device.hpp"
@@ -57,37 +55,12 @@ __device__ __forceinline__ float dot16<bf16_t>(const uint4 &q, const uint4 &k, f
     return acc;
 }
 
-// Descending bitonic sort of E*64 floats; element e*64 + lane is v[e].
-template <int E>
-__device__ __forceinline__ void wave_sort_desc(float (&v)[E], int lane)
+// Sum over the 4 lanes of a quad (DPP quad permutations, no LDS round trip).
+__device__ __forceinline__ float quad_sum(float x)
 {
-#pragma unroll
-    for (int kk = 2; kk <= 64 * E; kk <<= 1) {
-#pragma unroll
-        for (int j = kk >> 1; j > 0; j >>= 1) {
-            if (j >= 64) {
-                const int je = j >> 6;
-#pragma unroll
-                for (int e = 0; e < E; ++e) {
-                    if ((e & je) == 0) {
-                        const int e2 = e | je;
-                        const bool desc = (((e << 6) | lane) & kk) == 0;
-                        const float x = v[e], y = v[e2];
-                        v[e] = desc ? fmaxf(x, y) : fminf(x, y);
-                        v[e2] = desc ? fminf(x, y) : fmaxf(x, y);
-                    }
-                }
-            } else {
-#pragma unroll
-                for (int e = 0; e < E; ++e) {
-                    const float p = __shfl_xor(v[e], j, 64);
-                    const bool desc = (((e << 6) | lane) & kk) == 0;
-                    const bool lower = (lane & j) == 0;
-                    v[e] = (desc == lower) ? fmaxf(v[e], p) : fminf(v[e], p);
-                }
-            }
-        }
-    }
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));  // lane ^ 1
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));  // lane ^ 2
+    return x;
 }
 
 template <typename DT, int D, int E>
@@ -96,9 +69,12 @@ __global__ __launch_bounds__(256) void rescore_kernel(RescoreArgs a)
     constexpr int ROWB = D * (int)sizeof(DT);
     constexpr int CH = ROWB / 64;  // 16-byte pieces per lane (4 lanes per candidate)
     static_assert(CH >= 1 && ROWB % 64 == 0, "row bytes must be a multiple of 64");
-    constexpr int RB = (16 / CH) < 4 ? ((16 / CH) < 1 ? 1 : 16 / CH) : 4;  // rounds per batch
-    constexpr int NR = 4 * E;                                             // max rounds
-    constexpr int RPW = kRescoreRows / 4;                                 // rows per wave
+    constexpr int NR = 4 * E;               // rounds of 16 candidates
+    constexpr int RPW = kRescoreRows / 4;   // rows per wave
+    constexpr int SC = 64 * E + 1;          // LDS score row stride
+
+    __shared__ float sc[4][RPW][SC];
+    __shared__ int s_ncand[4][RPW], s_nsent[4][RPW];
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int G = lane >> 2, p = lane & 3;
@@ -108,9 +84,9 @@ __global__ __launch_bounds__(256) void rescore_kernel(RescoreArgs a)
     const int group = a.n_heads / a.n_kv_heads;
     const int c_sent = a.m + a.r, c_led = a.k + c_sent;
     const int rounds = (c_led + 15) >> 4;
-    const int T = a.k + a.m;
     const unsigned char *Kg = reinterpret_cast<const unsigned char *>(a.K) + (int64_t)(h / group) * a.n_k * ROWB;
     const unsigned char *Qb = reinterpret_cast<const unsigned char *>(a.Q);
+    const int nrows = min(RPW, a.n_q - i0);
 
     auto load_ids = [&](int64_t row, int (&idr)[E]) {
 #pragma unroll
@@ -128,117 +104,90 @@ __global__ __launch_bounds__(256) void rescore_kernel(RescoreArgs a)
 #pragma unroll
         for (int c = 0; c < CH; ++c) qv[c] = *reinterpret_cast<const uint4 *>(Qb + row * ROWB + (c * 4 + p) * 16);
     };
+    // Scores of one row (NR rounds, all loads issued before the first product)
+    // into sc[wave][q][slot]; an empty R slot reads +inf and an empty sentinel
+    // slot -inf, so neither can be the minimum over R or the maximum over C.
+    auto score_row = [&](int q, const int (&idr)[E], const uint4 (&qv)[CH]) {
+        int ids[NR];
+        uint4 kv[NR][CH];
+#pragma unroll
+        for (int u = 0; u < NR; ++u) {
+            const int slot = u * 16 + G;
+            ids[u] = (u < rounds) ? __shfl(idr[u >> 2], slot & 63, 64) : -1;
+            if (ids[u] >= 0) {
+                const unsigned char *kp = Kg + (int64_t)ids[u] * ROWB;
+#pragma unroll
+                for (int c = 0; c < CH; ++c) kv[u][c] = *reinterpret_cast<const uint4 *>(kp + (c * 4 + p) * 16);
+            }
+        }
+        int ncand = 0, nsent = 0;
+#pragma unroll
+        for (int u = 0; u < NR; ++u) {
+            const int slot = u * 16 + G;
+            float part = 0.0f;
+            if (ids[u] >= 0) {
+#pragma unroll
+                for (int c = 0; c < CH; ++c) part = dot16<DT>(qv[c], kv[u][c], part);
+            }
+            part = quad_sum(part);
+            if (p == 0 && u < rounds) sc[wave][q][slot] = (ids[u] >= 0) ? part : (slot < a.k ? INFINITY : -INFINITY);
+            ncand += __popcll(__ballot(ids[u] >= 0 && p == 0));
+            nsent += __popcll(__ballot(ids[u] >= 0 && p == 0 && slot >= a.k));
+        }
+        if (lane == 0) {
+            s_ncand[wave][q] = ncand;
+            s_nsent[wave][q] = nsent;
+        }
+    };
 
-    unsigned long long pairs_w = 0;
-    unsigned cnt_w = 0;
-    int idr[E], idn[E];
-    uint4 qv[CH], qn[CH];
-    const int nrows = min(RPW, a.n_q - i0);
+    int idr[E];
+    uint4 qv[CH];
     if (nrows > 0) {
         load_ids((int64_t)h * a.n_q + i0, idr);
         load_q((int64_t)h * a.n_q + i0, qv);
     }
     for (int q = 0; q < nrows; ++q) {
-        const int i = i0 + q;
-        const int64_t row = (int64_t)h * a.n_q + i;
-        float sc[NR];
-        // gathers of all rounds, RB rounds in flight at a time
-#pragma unroll
-        for (int u0 = 0; u0 < NR; u0 += RB) {
-            uint4 kv[RB][CH];
-            int ids[RB];
-#pragma unroll
-            for (int b = 0; b < RB; ++b) {
-                const int u = u0 + b;
-                const int slot = u * 16 + G;
-                ids[b] = (u < rounds) ? __shfl(idr[u >> 2], slot & 63, 64) : -1;
-                if (ids[b] >= 0) {
-                    const unsigned char *kp = Kg + (int64_t)ids[b] * ROWB;
-#pragma unroll
-                    for (int c = 0; c < CH; ++c) kv[b][c] = *reinterpret_cast<const uint4 *>(kp + (c * 4 + p) * 16);
-                }
-            }
-            if (u0 == 0 && q + 1 < nrows) {
-                load_ids(row + 1, idn);
-                load_q(row + 1, qn);
-            }
-#pragma unroll
-            for (int b = 0; b < RB; ++b) {
-                float part = 0.0f;
-                if (ids[b] >= 0) {
-#pragma unroll
-                    for (int c = 0; c < CH; ++c) part = dot16<DT>(qv[c], kv[b][c], part);
-                }
-                part += __shfl_xor(part, 1, 64);
-                part += __shfl_xor(part, 2, 64);
-                sc[u0 + b] = (ids[b] >= 0) ? part : NAN;
-            }
+        int idn[E];
+        uint4 qn[CH];
+        if (q + 1 < nrows) {
+            load_ids((int64_t)h * a.n_q + i0 + q + 1, idn);
+            load_q((int64_t)h * a.n_q + i0 + q + 1, qn);
         }
-        float amin = INFINITY, bmax = -INFINITY;
-        int ncand = 0;
-        bool has_c = false;
-#pragma unroll
-        for (int u = 0; u < NR; ++u) {
-            const int slot = u * 16 + G;
-            const bool valid = (u < rounds) && !isnan(sc[u]);
-            if (valid) {
-                if (slot < a.k)
-                    amin = fminf(amin, sc[u]);
-                else
-                    bmax = fmaxf(bmax, sc[u]);
-            }
-            const uint64_t mv = __ballot(valid && p == 0);
-            const uint64_t mc = __ballot(valid && p == 0 && slot >= a.k);
-            ncand += __popcll(mv);
-            has_c |= (mc != 0ull);
-        }
-#pragma unroll
-        for (int off = 4; off < 64; off <<= 1) {
-            amin = fminf(amin, __shfl_xor(amin, off, 64));
-            bmax = fmaxf(bmax, __shfl_xor(bmax, off, 64));
-        }
-        const bool flag = has_c && (bmax + a.gamma >= amin);
-        float theta = -INFINITY;
-        if (flag) {
-            // one score per lane (slot e*64 + lane), then the (k+m)-th best
-            float v[E];
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-                const int src = 4 * (lane & 15);
-                float x = NAN;
-#pragma unroll
-                for (int b = 0; b < 4; ++b) {
-                    const float y = __shfl(sc[4 * e + b], src, 64);
-                    x = ((lane >> 4) == b) ? y : x;
-                }
-                v[e] = (idr[e] >= 0 && !isnan(x)) ? x : -INFINITY;
-            }
-            wave_sort_desc<E>(v, lane);
-            if (ncand >= T) {
-                float t = -INFINITY;
-#pragma unroll
-                for (int e = 0; e < E; ++e)
-                    if (((T - 1) >> 6) == e) t = v[e];
-                theta = __shfl(t, (T - 1) & 63, 64);
-            }
-        }
-        if (lane == 0) {
-            a.flags[row] = flag ? 1 : 0;
-            if (a.mask_out) a.mask_out[row] = flag ? 1 : 0;
-            a.alpha[row] = amin;
-            a.beta[row] = bmax;
-            a.theta[row] = theta;
-            if (!flag) a.led_age[row] = a.layer - a.led_build[row];
-            const int ni = a.causal ? min(i + 1, a.n_k) : a.n_k;
-            pairs_w += (unsigned long long)(ncand + (flag ? ni : 0));
-            cnt_w += flag ? 1u : 0u;
-        }
+        score_row(q, idr, qv);
         if (q + 1 < nrows) {
 #pragma unroll
             for (int e = 0; e < E; ++e) idr[e] = idn[e];
 #pragma unroll
             for (int c = 0; c < CH; ++c) qv[c] = qn[c];
         }
+    }
+    __syncthreads();
+
+    // One lane per row: alpha, beta, the trigger, age, counts.
+    unsigned long long pairs_w = 0;
+    unsigned cnt_w = 0;
+    if (lane < nrows) {
+        const int i = i0 + lane;
+        const int64_t row = (int64_t)h * a.n_q + i;
+        const float *rs = sc[wave][lane];
+        float amin = INFINITY, bmax = -INFINITY;
+        for (int slot = 0; slot < a.k; ++slot) amin = fminf(amin, rs[slot]);
+        for (int slot = a.k; slot < c_led; ++slot) bmax = fmaxf(bmax, rs[slot]);
+        const int ncand = s_ncand[wave][lane], nsent = s_nsent[wave][lane];
+        const bool flag = nsent > 0 && (bmax + a.gamma >= amin);
+        a.flags[row] = flag ? 1 : 0;
+        if (a.mask_out) a.mask_out[row] = flag ? 1 : 0;
+        a.alpha[row] = amin;
+        a.beta[row] = bmax;
+        if (!flag) a.led_age[row] = a.layer - a.led_build[row];
+        const int ni = a.causal ? min(i + 1, a.n_k) : a.n_k;
+        pairs_w = (unsigned long long)(ncand + (flag ? ni : 0));
+        cnt_w = flag ? 1u : 0u;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        pairs_w += (unsigned long long)__shfl_xor((long long)pairs_w, off, 64);
+        cnt_w += (unsigned)__shfl_xor((int)cnt_w, off, 64);
     }
 
     __shared__ unsigned long long s_pairs[4];
@@ -264,9 +213,10 @@ __global__ __launch_bounds__(256) void rescore_kernel(RescoreArgs a)
         const unsigned long long P = __hip_atomic_load(a.acc_pairs, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         const int tr = a.reroute_tile_rows;
         int base = 0, total = 0;
-        for (int hd = 0; hd < a.n_heads; ++hd) {
+        for (int j = 0; j < a.n_heads; ++j) {
+            const int hd = head_at(j, a.n_heads, a.n_kv_heads);
             const unsigned c = __hip_atomic_load(&a.acc_count[hd], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            a.tile_base[hd] = base;
+            a.tile_base[j] = base;
             base += (int)((c + tr - 1) / tr);
             total += (int)c;
             a.acc_count[hd] = 0u;

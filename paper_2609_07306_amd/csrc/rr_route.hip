@@ -4,10 +4,8 @@
 
 namespace rr {
 
-hipError_t launch_route_f32_w2(const RouteArgs &a, int grid, hipStream_t stream);
-hipError_t launch_route_f32_w4(const RouteArgs &a, int grid, hipStream_t stream);
-hipError_t launch_route_bf16_w2(const RouteArgs &a, int grid, hipStream_t stream);
-hipError_t launch_route_bf16_w4(const RouteArgs &a, int grid, hipStream_t stream);
+hipError_t launch_route_f32(const RouteArgs &a, int grid, hipStream_t stream);
+hipError_t launch_route_bf16(const RouteArgs &a, int grid, hipStream_t stream);
 
 bool route_supported(int dtype, int d, int T)
 {
@@ -17,14 +15,12 @@ bool route_supported(int dtype, int d, int T)
     return false;
 }
 
-int route_tile_rows(int mode) { return mode == MODE_REROUTE ? 32 * kRerouteWaves : 32 * kFullWaves; }
+int route_tile_rows(int T) { return T > 64 ? kWideTileRows : kNarrowTileRows; }
 
 hipError_t launch_route(const RouteArgs &a, int dtype, int grid, hipStream_t stream)
 {
-    static_assert(kRerouteWaves == 2 && kFullWaves == 4, "instantiated tile widths");
-    const bool reroute = a.mode == MODE_REROUTE;
-    if (dtype == 0) return reroute ? launch_route_f32_w2(a, grid, stream) : launch_route_f32_w4(a, grid, stream);
-    return reroute ? launch_route_bf16_w2(a, grid, stream) : launch_route_bf16_w4(a, grid, stream);
+    if (dtype == 0) return launch_route_f32(a, grid, stream);
+    return launch_route_bf16(a, grid, stream);
 }
 
 }  // namespace rr

@@ -50,6 +50,9 @@ FULL_CASES = [
     ("bf16_d256", 2, 2, 64, 96, 256, "bf16", 12, False),
     ("bf16_d32_k_eq_nk", 1, 1, 40, 20, 32, "bf16", 20, False),
     ("wide_k", 2, 2, 64, 512, 128, "bf16", 100, False),
+    # rows just past a tile boundary of a causal head: one half of the key
+    # range holds nearly every valid chunk, so its sub-list overflows
+    ("causal_overflow_k48", 8, 2, 256, 256, 128, "bf16", 48, True),
 ]
 
 
@@ -139,6 +142,67 @@ def test_all_zero_scores_pick_lowest_ids():
     L.close()
 
 
+@pytest.mark.parametrize("T_class", ["narrow", "wide"])
+@pytest.mark.parametrize("causal", [False, True])
+def test_ledger_exact_ties_integer_data(T_class, causal):
+    """Anchor, then a relay, on small-integer inputs: every score is exact in
+    binary32 on both sides, so the whole ledger (routes, near-miss and random
+    sentinels, ages), the mask and alpha / beta must match the oracle on every
+    row.  Massive exact ties make the collection sub-lists overflow, which
+    drives the bisection repair and its (score, id) tie cut."""
+    from parity_util import dev, ledger_np
+    rr = rrmod()
+    rng = np.random.default_rng(11 if causal else 12)
+    H, n, d = 2, 300, 32
+    k, m, r = (24, 12, 8) if T_class == "narrow" else (60, 30, 20)
+    note(f"integer-tie ledger: {T_class} causal={causal}")
+    p = oracle.Problem(H, H, n, n, d, k, m, r, causal, seed=7)
+    cfg = rr.Config(H, H, n, n, d, k, m, r, "f32", causal, seed=7)
+    L = rr.Ledger(cfg)
+    ref = oracle.new_ledger(p)
+    for layer in range(3):
+        Q = rng.integers(-2, 3, size=(H, n, d)).astype(np.float32)
+        K = rng.integers(-1, 2, size=(H, n, d)).astype(np.float32)
+        if layer == 0:
+            L.anchor(layer, dev(Q, "f32"), dev(K, "f32"))
+            oracle.anchor(p, layer, Q, K, ref)
+        else:
+            mask = torch.empty(cfg.rows, dtype=torch.uint8, device="cuda")
+            L.relay(layer, dev(Q, "f32"), dev(K, "f32"), mask=mask)
+            out = oracle.relay(p, layer, Q, K, ref)
+            np.testing.assert_array_equal(mask.cpu().numpy(), out["mask"])
+            alpha, beta, _ = L.relay_stats()
+            np.testing.assert_array_equal(alpha.cpu().numpy(), out["alpha"].astype(np.float32))
+            np.testing.assert_array_equal(beta.cpu().numpy(), out["beta"].astype(np.float32))
+        got = ledger_np(L)
+        for key in ("routes", "sent", "build", "age"):
+            np.testing.assert_array_equal(got[key], ref[key], err_msg=f"layer {layer} {key}")
+    L.close()
+
+
+@pytest.mark.parametrize("n,k,m,r,causal", [(600, 10, 5, 5, False), (600, 40, 60, 16, True),
+                                            (1000, 32, 16, 16, True)])
+def test_all_zero_scores_overflow(n, k, m, r, causal):
+    """All scores zero: every chunk reaches every threshold, both sub-lists
+    overflow, and the result is the lowest ids (R = 0..k-1, N = k..k+m-1)."""
+    from parity_util import dev, ledger_np
+    rr = rrmod()
+    H, d = 2, 64
+    note(f"all-zero overflow: n={n} k={k} m={m} r={r} causal={causal}")
+    Q = np.zeros((H, n, d), np.float32)
+    K = np.random.default_rng(3).standard_normal((H, n, d)).astype(np.float32)
+    p = oracle.Problem(H, H, n, n, d, k, m, r, causal)
+    cfg = rr.Config(H, H, n, n, d, k, m, r, "f32", causal)
+    L = rr.Ledger(cfg)
+    L.anchor(0, dev(Q, "f32"), dev(K, "f32"))
+    got = ledger_np(L)
+    ref = oracle.new_ledger(p)
+    oracle.anchor(p, 0, Q, K, ref)
+    for key in ("routes", "sent", "build", "age"):
+        np.testing.assert_array_equal(got[key], ref[key], err_msg=key)
+    L.close()
+
+
 # ------------------------------------------------------- rollout parity
 
 ROLLOUTS = [
@@ -210,6 +274,8 @@ FULL_SIZE = [
     ("gqa", {}),
     ("drift", {"rho": 0.3}),
     ("longctx", {}),
+    ("scale", {"n": 8192, "n_heads": 2, "n_kv_heads": 2}),
+    ("longctx", {"n": 8192, "n_heads": 2, "n_kv_heads": 2}),
 ]
 
 
