@@ -13,6 +13,10 @@ typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 // Storage tag of bf16 inputs (the bits are read as __bf16 vectors).
+// Four 32-bit lanes loaded or stored as one 16-byte vector (a native vector
+// type, so arrays of them stay in registers).
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
 struct bf16_t {
     uint16_t bits;
 };
