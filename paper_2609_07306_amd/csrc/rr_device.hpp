@@ -83,6 +83,16 @@ __device__ __forceinline__ uint64_t sm64(uint64_t z)
     return z ^ (z >> 31);
 }
 
+// Workgroup barrier that orders LDS only: it waits for this wave's LDS
+// operations but not for its outstanding global stores, which no thread of
+// the workgroup reads back.
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // --------------------------------------------------------------- fragments
 //
 // One lane of a 32x32 MFMA holds, for its row (A) or column (B) lane%32, the
@@ -123,6 +133,12 @@ struct Frag<float, D> {
         for (int s = 0; s < NS; ++s) c = __builtin_amdgcn_mfma_f32_32x32x2f32(a.v[s], b.v[s], c, 0, 0, 0);
         return c;
     }
+
+    // step s of the product (s a compile-time constant after unrolling)
+    __device__ __forceinline__ static f32x16_t mma_step(const Frag &a, const Frag &b, f32x16_t c, int s)
+    {
+        return __builtin_amdgcn_mfma_f32_32x32x2f32(a.v[s], b.v[s], c, 0, 0, 0);
+    }
 };
 
 template <int D>
@@ -151,6 +167,12 @@ struct Frag<bf16_t, D> {
 #pragma unroll
         for (int s = 0; s < NS; ++s) c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.v[s], b.v[s], c, 0, 0, 0);
         return c;
+    }
+
+    // step s of the product (s a compile-time constant after unrolling)
+    __device__ __forceinline__ static f32x16_t mma_step(const Frag &a, const Frag &b, f32x16_t c, int s)
+    {
+        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a.v[s], b.v[s], c, 0, 0, 0);
     }
 };
 
