@@ -17,11 +17,11 @@ struct rr_ledger {
     bool has_state;
     int32_t last_layer;
     int64_t rows;
-    int32_t *routes, *sent, *build, *age, *ids, *tile_base, *stat_nrr;
+    int32_t *routes, *sent, *build, *age, *ids, *stat_nrr;
     uint8_t *flags;
     float *alpha, *beta;
-    unsigned long long *acc_pairs;
-    uint32_t *acc_count, *ticket;
+    int64_t *blk_pairs;  // rescoring workgroup partials, consumed by the reroute kernel
+    int32_t *blk_count;
     int64_t *stat_pairs;
 };
 
@@ -70,6 +70,7 @@ rr_status validate(const rr_config *c, bool ledger)
         return fail(RR_ERR_UNSUPPORTED, "unsupported (dtype, d, k+m): d in {32,64,128} (256 for bf16), k+m <= 128");
     if (c->k + m + r > 256) return fail(RR_ERR_UNSUPPORTED, "k + m + r must be <= 256");
     if (c->n_k > 8192) return fail(RR_ERR_UNSUPPORTED, "n_k must be <= 8192");
+    if (c->n_heads > 1024) return fail(RR_ERR_UNSUPPORTED, "n_heads must be <= 1024");
     if (rows_of(*c) * (int64_t)(c->k + m + r + 1) >= (int64_t)INT32_MAX || rows_of(*c) * c->d >= (int64_t)INT32_MAX * 8)
         return fail(RR_ERR_UNSUPPORTED, "problem too large for 32-bit row indexing");
     return RR_OK;
@@ -104,9 +105,8 @@ rr_status alloc(T **p, int64_t n, const char *what)
 
 void free_all(rr_ledger *L)
 {
-    void *ptrs[] = {L->routes, L->sent,  L->build, L->age,       L->ids,       L->tile_base,
-                    L->stat_nrr, L->flags, L->alpha, L->beta, L->acc_pairs,
-                    L->acc_count, L->ticket, L->stat_pairs};
+    void *ptrs[] = {L->routes, L->sent,  L->build,     L->age,       L->ids,       L->stat_nrr,
+                    L->flags,  L->alpha, L->beta,      L->blk_pairs, L->blk_count, L->stat_pairs};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);
 }
@@ -217,26 +217,23 @@ rr_status rr_ledger_create(const rr_config *cfg, rr_ledger **out)
         return fail(RR_ERR_HIP, "hipGetDevice failed");
     }
     const int64_t rows = L->rows;
-    const int H = cfg->n_heads;
+    // rescoring workgroups: at most one per 8 rows of a head
+    const int64_t max_blocks = (int64_t)cfg->n_heads * ((cfg->n_q + rr::kRescoreWaves - 1) / rr::kRescoreWaves);
     if ((st = alloc(&L->routes, rows * cfg->k, "routes")) != RR_OK ||
         (st = alloc(&L->sent, rows * (cfg->m + cfg->r), "sentinels")) != RR_OK ||
         (st = alloc(&L->build, rows, "build")) != RR_OK || (st = alloc(&L->age, rows, "age")) != RR_OK ||
-        (st = alloc(&L->ids, rows, "ids")) != RR_OK || (st = alloc(&L->tile_base, H + 1, "tile_base")) != RR_OK ||
-        (st = alloc(&L->stat_nrr, 1, "stat_nrr")) != RR_OK || (st = alloc(&L->flags, rows, "flags")) != RR_OK ||
-        (st = alloc(&L->alpha, rows, "alpha")) != RR_OK || (st = alloc(&L->beta, rows, "beta")) != RR_OK ||
-        (st = alloc(&L->acc_pairs, 1, "acc_pairs")) != RR_OK ||
-        (st = alloc(&L->acc_count, H, "acc_count")) != RR_OK || (st = alloc(&L->ticket, 1, "ticket")) != RR_OK ||
+        (st = alloc(&L->ids, rows, "ids")) != RR_OK || (st = alloc(&L->stat_nrr, 1, "stat_nrr")) != RR_OK ||
+        (st = alloc(&L->flags, rows, "flags")) != RR_OK || (st = alloc(&L->alpha, rows, "alpha")) != RR_OK ||
+        (st = alloc(&L->beta, rows, "beta")) != RR_OK ||
+        (st = alloc(&L->blk_pairs, max_blocks, "rescore partials")) != RR_OK ||
+        (st = alloc(&L->blk_count, max_blocks, "rescore counts")) != RR_OK ||
         (st = alloc(&L->stat_pairs, 1, "stat_pairs")) != RR_OK) {
         free_all(L);
         delete L;
         return st;
     }
-    // One-time initialisation (outside any hot path): the accumulators and
-    // ticket of the rescoring kernel start at zero and are left at zero by it.
-    hipError_t e = hipMemset(L->acc_pairs, 0, sizeof(unsigned long long));
-    if (e == hipSuccess) e = hipMemset(L->acc_count, 0, sizeof(uint32_t) * H);
-    if (e == hipSuccess) e = hipMemset(L->ticket, 0, sizeof(uint32_t));
-    if (e == hipSuccess) e = hipMemset(L->tile_base, 0, sizeof(int32_t) * (H + 1));
+    // One-time initialisation (outside any hot path): an empty ledger.
+    hipError_t e = hipSuccess;
     if (e == hipSuccess) e = hipMemset(L->routes, 0xFF, sizeof(int32_t) * rows * cfg->k);
     if (e == hipSuccess && cfg->m + cfg->r > 0) e = hipMemset(L->sent, 0xFF, sizeof(int32_t) * rows * (cfg->m + cfg->r));
     if (e == hipSuccess) e = hipMemset(L->build, 0xFF, sizeof(int32_t) * rows);
@@ -313,9 +310,12 @@ rr_status rr_relay_layer(rr_ledger *L, int32_t layer, const void *Qc, const void
     s.r = c.r;
     s.causal = c.causal;
     s.layer = layer;
-    s.blocks_per_head = (c.n_q + rr::kRescoreRows - 1) / rr::kRescoreRows;
+    rr::RescoreGeometry geo;
+    rr::rescore_geometry(c.dtype, c.d, c.n_k, L->rows, c.k + c.m + c.r, c.n_q, geo);
+    s.blocks_per_head = geo.blocks_per_head;
+    s.rows_per_wave = geo.rows_per_wave;
+    s.pieces = geo.pieces;
     s.gamma = c.gamma;
-    s.reroute_tile_rows = rr::route_tile_rows(c.k + c.m);
     s.led_routes = L->routes;
     s.led_sent = L->sent;
     s.led_build = L->build;
@@ -324,15 +324,9 @@ rr_status rr_relay_layer(rr_ledger *L, int32_t layer, const void *Qc, const void
     s.mask_out = mask;
     s.alpha = L->alpha;
     s.beta = L->beta;
-    s.acc_pairs = L->acc_pairs;
-    s.acc_count = L->acc_count;
-    s.ticket = L->ticket;
-    s.tile_base = L->tile_base;
-    s.stat_pairs = L->stat_pairs;
-    s.stat_nrr = L->stat_nrr;
-    s.pairs_out = pairs;
-    s.nrr_out = n_rerouted;
-    hipError_t e = timed(RR_KERNEL_RESCORE, stream, [&] { return rr::launch_rescore(s, c.dtype, stream); });
+    s.blk_pairs = L->blk_pairs;
+    s.blk_count = L->blk_count;
+    hipError_t e = timed(RR_KERNEL_RESCORE, stream, [&] { return rr::launch_rescore(s, c.dtype, geo.lds_bytes, stream); });
     if (e != hipSuccess) return hip_fail(e, "rescore launch");
 
     rr::RouteArgs a = route_args(c, Qc, Kc);
@@ -343,7 +337,13 @@ rr_status rr_relay_layer(rr_ledger *L, int32_t layer, const void *Qc, const void
     a.led_build = L->build;
     a.led_age = L->age;
     a.flags = L->flags;
-    a.tile_base = L->tile_base;
+    a.blk_count = L->blk_count;
+    a.blk_pairs = L->blk_pairs;
+    a.rescore_bph = geo.blocks_per_head;
+    a.stat_pairs = L->stat_pairs;
+    a.stat_nrr = L->stat_nrr;
+    a.pairs_out = pairs;
+    a.nrr_out = n_rerouted;
     a.ids_out = L->ids;
     const int rt = rr::route_tile_rows(c.k + c.m);
     const int max_tiles = c.n_heads * ((c.n_q + rt - 1) / rt);

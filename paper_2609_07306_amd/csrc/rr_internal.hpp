@@ -14,7 +14,9 @@ enum RouteMode : int32_t {
 
 constexpr int kNarrowTileRows = 128;  // route tile rows when k + m <= 64
 constexpr int kWideTileRows = 64;     // route tile rows when 64 < k + m <= 128
-constexpr int kRescoreRows = 32;  // rows per rescoring workgroup (4 waves)
+constexpr int kRescoreWaves = 8;              // waves per rescoring workgroup
+constexpr int kRescoreSlotRows = 16;          // rows x 64-slot groups a rescoring wave holds in registers
+constexpr int kRescoreKeyBudget = 64 * 1024;  // LDS bytes of one staged key slice (n_k <= 4096)
 
 struct RouteArgs {
     const void *Q;
@@ -34,10 +36,16 @@ struct RouteArgs {
     int32_t *led_build;
     int32_t *led_age;
     const uint8_t *flags;      // reroute: [rows]
-    const int32_t *tile_base;  // reroute: [n_heads + 1] tile offsets, XCD-major head order
+    const int32_t *blk_count;  // reroute: flagged rows per rescoring workgroup, head-major
+    const int64_t *blk_pairs;  // reroute: score pairs per rescoring workgroup, head-major
+    int32_t rescore_bph;       // reroute: rescoring workgroups per head
+    int32_t lds_tiles;         // reroute: LDS byte offset of the per-head tile table (set by the launcher)
+    int64_t *stat_pairs;       // reroute: the call's score pairs (ledger copy)
+    int32_t *stat_nrr;         // reroute: the call's rerouted rows (ledger copy)
+    int32_t *nrr_out;          // reroute: optional device scalar
     int32_t *ids_out;          // reroute: compacted row ids per head, or null
     int64_t *pairs_out;        // optional device scalar
-    int64_t pairs_value;       // value written to pairs_out (full / anchor)
+    int64_t pairs_value;       // value written to pairs_out (full / anchor; reroute: the workgroup sums)
 };
 
 struct RescoreArgs {
@@ -47,8 +55,9 @@ struct RescoreArgs {
     int32_t k, m, r;
     int32_t causal;
     int32_t layer;
-    int32_t blocks_per_head;  // ceil(n_q / kRescoreRows)
-    int32_t reroute_tile_rows;
+    int32_t blocks_per_head;  // ceil(n_q / rows per block)
+    int32_t rows_per_wave;    // rows per block = kRescoreWaves * rows_per_wave
+    int32_t pieces;           // 16-byte pieces of each key row staged per pass (power of two)
     float gamma;
     const int32_t *led_routes;
     const int32_t *led_sent;
@@ -58,20 +67,20 @@ struct RescoreArgs {
     uint8_t *mask_out;  // [rows] caller mask or null
     float *alpha;
     float *beta;
-    unsigned long long *acc_pairs;  // zero between calls
-    uint32_t *acc_count;            // [n_heads], zero between calls
-    uint32_t *ticket;               // zero between calls
-    int32_t *tile_base;             // [n_heads + 1] written by the last block
-    int64_t *stat_pairs;
-    int32_t *stat_nrr;
-    int64_t *pairs_out;  // optional
-    int32_t *nrr_out;    // optional
+    int64_t *blk_pairs;  // [n_heads * blocks_per_head] score pairs per workgroup (head-major)
+    int32_t *blk_count;  // [n_heads * blocks_per_head] flagged rows per workgroup
 };
 
 // Supported (dtype, d) combinations; dtype 0 = binary32, 1 = bf16.
 bool route_supported(int dtype, int d, int T);
 int route_tile_rows(int T);  // query rows per route tile for T = k + m
 hipError_t launch_route(const RouteArgs &a, int dtype, int grid, hipStream_t stream);
-hipError_t launch_rescore(const RescoreArgs &a, int dtype, hipStream_t stream);
+// Launch shape of the rescoring kernel for a configuration.
+struct RescoreGeometry {
+    int pieces, rows_per_wave, rows_per_block, blocks_per_head;
+    size_t lds_bytes;
+};
+void rescore_geometry(int dtype, int d, int n_k, int64_t rows, int c, int n_q, RescoreGeometry &g);
+hipError_t launch_rescore(const RescoreArgs &a, int dtype, size_t lds, hipStream_t stream);
 
 }  // namespace rr
