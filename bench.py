@@ -32,6 +32,33 @@ if ROOT not in sys.path:
 
 PEAK = {"hbm": 8000.0, "mfma_bf16": 2500.0, "mfma_f32": 157.3}  # GB/s, TFLOP/s
 
+# HBM bytes per launch of the dominant kernel, from byte-counter passes
+# (FETCH_SIZE, WRITE_SIZE, calibrated on a copy of known size) recorded in
+# this profile; valid only while the kernel's sources hash to the recorded value.
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "route_rescore_scale_n1024_hbm_bytes.md")
+TRAFFIC_SOURCES = ["paper_2609_07306_amd/csrc/rr_route_impl.hpp", "paper_2609_07306_amd/csrc/rr_device.hpp",
+                   "paper_2609_07306_amd/csrc/rr_internal.hpp", "paper_2609_07306_amd/csrc/rr_route_bf16_reroute.hip",
+                   "paper_2609_07306_amd/build.py"]
+
+
+def recorded_traffic(kernel: str):
+    """Counter-measured HBM bytes per launch of `kernel`, or None if not recorded
+    or if the kernel's sources changed since the counters were taken."""
+    import hashlib
+    import re
+    try:
+        text = open(TRAFFIC_PROFILE).read()
+    except OSError:
+        return None
+    m = re.search(r"bench-traffic kernel=(\w+) bytes_per_launch=(\d+) sources_sha256=([0-9a-f]+)", text)
+    if not m or m.group(1) != kernel:
+        return None
+    h = hashlib.sha256()
+    for f in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return int(m.group(2)) if h.hexdigest() == m.group(3) else None
+
 
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
@@ -44,6 +71,8 @@ def parse():
     ap.add_argument("--cpu-heads", type=int, default=2, help="heads in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-full", action="store_true", help="skip the full-routing baseline")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a device-to-device copy of MIB MiB (calibrates the HBM byte counters)")
     return ap.parse_args()
 
 
@@ -78,6 +107,17 @@ def main():
         sys.exit(2)
     torch.cuda.set_device(0)
     dev = torch.device("cuda", 0)
+    if args.copy_calibration:
+        # one plain copy of a known size: the FETCH_SIZE / WRITE_SIZE counters
+        # of this dispatch give the scale factor of the byte counters
+        n = args.copy_calibration << 20
+        src = torch.ones(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n}))
+        return
 
     kw = {}
     if args.n:
@@ -218,8 +258,11 @@ def main():
             kernels[kind]["share_of_step"] = round(prof[kind][0] / args.steps / ms_step, 4)
     dom = max(("anchor", "reroute", "rescore"), key=lambda k: prof[k][0])
     dk = kernels[dom]
+    # the recorded counters belong to the default workload (routing scale, n = 1024)
+    default_workload = args.workload == "scale" and w.n == 1024 and args.rho is None
     roofline = {"kernel": dom, "bound": dk["bound"], "achieved": dk["achieved"], "peak": dk["peak"],
-                "unit": dk["unit"], "frac": dk["frac"], "traffic": None}
+                "unit": dk["unit"], "frac": dk["frac"],
+                "traffic": recorded_traffic(dom) if default_workload else None}
 
     value = rows * L / (ms_step * 1e-3)
     out = {

@@ -1,0 +1,11 @@
+// Route kernel instances: bf16 inputs, full routing.
+#include "rr_route_impl.hpp"
+
+namespace rr {
+
+hipError_t launch_route_bf16_full(const RouteArgs &a, int grid, hipStream_t stream)
+{
+    return route_detail::launch_family<MODE_FULL, bf16_t>(a, grid, stream);
+}
+
+}  // namespace rr
