@@ -217,7 +217,7 @@ rr_status rr_ledger_create(const rr_config *cfg, rr_ledger **out)
         return fail(RR_ERR_HIP, "hipGetDevice failed");
     }
     const int64_t rows = L->rows;
-    // rescoring workgroups: at most one per 8 rows of a head
+    // rescoring workgroups: at most one per kRescoreWaves rows of a head
     const int64_t max_blocks = (int64_t)cfg->n_heads * ((cfg->n_q + rr::kRescoreWaves - 1) / rr::kRescoreWaves);
     if ((st = alloc(&L->routes, rows * cfg->k, "routes")) != RR_OK ||
         (st = alloc(&L->sent, rows * (cfg->m + cfg->r), "sentinels")) != RR_OK ||
@@ -311,10 +311,9 @@ rr_status rr_relay_layer(rr_ledger *L, int32_t layer, const void *Qc, const void
     s.causal = c.causal;
     s.layer = layer;
     rr::RescoreGeometry geo;
-    rr::rescore_geometry(c.dtype, c.d, c.n_k, L->rows, c.k + c.m + c.r, c.n_q, geo);
+    rr::rescore_geometry(L->rows, c.n_q, geo);
     s.blocks_per_head = geo.blocks_per_head;
     s.rows_per_wave = geo.rows_per_wave;
-    s.pieces = geo.pieces;
     s.gamma = c.gamma;
     s.led_routes = L->routes;
     s.led_sent = L->sent;
@@ -326,7 +325,7 @@ rr_status rr_relay_layer(rr_ledger *L, int32_t layer, const void *Qc, const void
     s.beta = L->beta;
     s.blk_pairs = L->blk_pairs;
     s.blk_count = L->blk_count;
-    hipError_t e = timed(RR_KERNEL_RESCORE, stream, [&] { return rr::launch_rescore(s, c.dtype, geo.lds_bytes, stream); });
+    hipError_t e = timed(RR_KERNEL_RESCORE, stream, [&] { return rr::launch_rescore(s, c.dtype, stream); });
     if (e != hipSuccess) return hip_fail(e, "rescore launch");
 
     rr::RouteArgs a = route_args(c, Qc, Kc);

@@ -14,9 +14,9 @@ enum RouteMode : int32_t {
 
 constexpr int kNarrowTileRows = 128;  // route tile rows when k + m <= 64
 constexpr int kWideTileRows = 64;     // route tile rows when 64 < k + m <= 128
-constexpr int kRescoreWaves = 8;              // waves per rescoring workgroup
-constexpr int kRescoreSlotRows = 16;          // rows x 64-slot groups a rescoring wave holds in registers
-constexpr int kRescoreKeyBudget = 64 * 1024;  // LDS bytes of one staged key slice (n_k <= 4096)
+constexpr int kRescoreWaves = 4;            // waves per rescoring workgroup
+constexpr int kRescoreBlocks = 512;         // target rescoring workgroups per launch (two per CU)
+constexpr int kRescoreMaxRowsPerWave = 16;  // rows a rescoring wave scores in turn
 
 struct RouteArgs {
     const void *Q;
@@ -57,7 +57,6 @@ struct RescoreArgs {
     int32_t layer;
     int32_t blocks_per_head;  // ceil(n_q / rows per block)
     int32_t rows_per_wave;    // rows per block = kRescoreWaves * rows_per_wave
-    int32_t pieces;           // 16-byte pieces of each key row staged per pass (power of two)
     float gamma;
     const int32_t *led_routes;
     const int32_t *led_sent;
@@ -77,10 +76,9 @@ int route_tile_rows(int T);  // query rows per route tile for T = k + m
 hipError_t launch_route(const RouteArgs &a, int dtype, int grid, hipStream_t stream);
 // Launch shape of the rescoring kernel for a configuration.
 struct RescoreGeometry {
-    int pieces, rows_per_wave, rows_per_block, blocks_per_head;
-    size_t lds_bytes;
+    int rows_per_wave, rows_per_block, blocks_per_head;
 };
-void rescore_geometry(int dtype, int d, int n_k, int64_t rows, int c, int n_q, RescoreGeometry &g);
-hipError_t launch_rescore(const RescoreArgs &a, int dtype, size_t lds, hipStream_t stream);
+void rescore_geometry(int64_t rows, int n_q, RescoreGeometry &g);
+hipError_t launch_rescore(const RescoreArgs &a, int dtype, hipStream_t stream);
 
 }  // namespace rr

@@ -4,30 +4,25 @@
 // Each row's candidates are its ledger slots: R (k slots), then the near-miss
 // sentinels (m) and the random sentinels (r); -1 slots are empty.  Rescoring
 // is a sampled product: only the (row, slot) pairs named by the ledger are
-// scored, each as a dot product over d.
+// scored, each as a dot product over d, with the key rows gathered straight
+// from L2 (a head's key matrix is read by every workgroup of the head, and
+// the workgroup-to-head map keeps a key head's workgroups on one XCD).
 //
-// Gathering candidate key rows straight from L2 is bound by the vector L1's
-// request rate (every 256-byte key row is a separate random access), so a
-// workgroup instead stages its head's whole key matrix in LDS, one slice of
-// the d range at a time: pass p holds bytes [16 P p, 16 P (p+1)) of every key
-// row (P 16-byte pieces per key, P a power of two chosen so that n_k * P * 16
-// bytes fit the LDS budget), together with the same slice of the block's query
-// rows.  Lane j of a wave owns slot j (j + 64 e for the e-th group of 64 slots)
-// of the wave's current row and accumulates its dot over the pass's pieces.
-// The lanes of a wave read their pieces in a lane-rotated order (piece
-// (u + lane) mod P at step u): key rows are P * 16 bytes apart, so the 8 lanes
-// of an LDS access group read distinct 16-byte bank groups whatever the key
-// ids are (for P >= 8).  The partial dots stay in registers across passes.
-//
-// After the last pass, wave reductions over the slot lanes give each row
-// alpha = min over R, beta = max over C and its candidate count; one lane per
-// row forms the refresh flag (C non-empty and beta + gamma >= alpha), writes
-// the mask, alpha and beta, and sets age = layer - build layer on rows that
-// keep their route.  Each workgroup stores its flagged-row and score-pair
-// counts in its own slot of a per-workgroup table (no atomics); the reroute
-// kernel turns the table into its per-head tile list and the call's totals.
-// No host synchronisation.
+// A wave scores one row at a time: 16 candidates per round, 4 lanes per
+// candidate, each lane reading 16-byte pieces so that one load instruction
+// covers 64 contiguous bytes of 16 key rows; the loads of all rounds are in
+// flight before the first product, and the next row's slot ids and query are
+// already requested.  The 4 partial dots of a candidate are summed with two
+// DPP quad permutations.  Wave reductions (DPP row shifts and row
+// broadcasts) give the row's alpha = min over R, beta = max over C and its
+// candidate counts; one lane per row then forms the refresh flag (C
+// non-empty and beta + gamma >= alpha), writes the mask, alpha and beta, and
+// sets age = layer - build layer on rows that keep their route.  Each
+// workgroup stores its flagged-row and score-pair counts in its own slot of a
+// per-workgroup table (no atomics); the reroute kernel turns the table into
+// its per-head tile list and the call's totals.  No host synchronisation.
 #include <math.h>
+
 
 #include "rr_device.hpp"
 #include "rr_internal.hpp"
@@ -35,9 +30,7 @@
 namespace rr {
 namespace {
 
-constexpr int kWaves = kRescoreWaves;  // waves per workgroup
-constexpr int kThreads = 64 * kWaves;
-constexpr int kStageUnroll = 8;  // staging loads in flight per thread
+constexpr int kThreads = 64 * kRescoreWaves;
 
 template <typename DT>
 __device__ __forceinline__ float dot16(const u32x4_t &q, const u32x4_t &k, float acc);
@@ -66,153 +59,152 @@ __device__ __forceinline__ float dot16<bf16_t>(const u32x4_t &q, const u32x4_t &
     return acc;
 }
 
-// E groups of 64 slots per row; each wave scores up to RPW rows of the block
-// (the block holds rows_per_block = kWaves * rows_per_wave rows).
+// Minimum / maximum over the 64 lanes of a wave, returned to every lane:
+// shifts within each row of 16 lanes, then row broadcasts carry rows 0..2
+// into lane 63, which is read back as a scalar.
+// Sum over the 4 lanes of a quad (DPP quad permutations, no LDS round trip).
+__device__ __forceinline__ float quad_sum(float x)
+{
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));  // lane ^ 1
+    x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));  // lane ^ 2
+    return x;
+}
+
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_move(float fill, float x)
+{
+    return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(fill), __float_as_int(x), CTRL, ROW_MASK, 0xF, false));
+}
+
+template <bool MIN>
+__device__ __forceinline__ float wave_extremum(float v)
+{
+    constexpr float id = MIN ? INFINITY : -INFINITY;
+    auto op = [](float a, float b) { return MIN ? fminf(a, b) : fmaxf(a, b); };
+    v = op(v, dpp_move<0x111, 0xF>(id, v));  // row_shr:1
+    v = op(v, dpp_move<0x112, 0xF>(id, v));  // row_shr:2
+    v = op(v, dpp_move<0x114, 0xF>(id, v));  // row_shr:4
+    v = op(v, dpp_move<0x118, 0xF>(id, v));  // row_shr:8: lane 15 of a row holds the row
+    v = op(v, dpp_move<0x142, 0xA>(id, v));  // row_bcast:15 into rows 1, 3
+    v = op(v, dpp_move<0x143, 0xC>(id, v));  // row_bcast:31 into rows 2, 3
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+// E groups of 64 slots per row; a block of kRescoreWaves waves scores
+// rows_per_wave consecutive rows per wave.
 template <typename DT, int D, int E>
 __global__ __launch_bounds__(kThreads) void rescore_kernel(RescoreArgs a)
 {
     constexpr int ROWB = D * (int)sizeof(DT);
-    constexpr int DP = ROWB / 16;        // 16-byte pieces per key row
-    constexpr int RPW = kRescoreSlotRows / E;  // register budget: RPW * E partial dots per lane
-    static_assert(ROWB % 16 == 0, "key rows are whole 16-byte pieces");
+    constexpr int CH = ROWB / 64;  // 16-byte pieces per lane (4 lanes per candidate)
+    static_assert(CH >= 1 && ROWB % 64 == 0, "row bytes must be a multiple of 64");
+    constexpr int NR = 4 * E;      // rounds of 16 candidates
+    constexpr int NWG = kRescoreWaves;
 
-    extern __shared__ __align__(16) unsigned char smem[];
-    __shared__ unsigned long long s_pairs[kWaves];
-    __shared__ unsigned s_cnt[kWaves];
+    __shared__ unsigned long long s_pairs[NWG];
+    __shared__ unsigned s_cnt[NWG];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int G = lane >> 2, pq = lane & 3;
     int h, blk;
     tile_of_block(blockIdx.x, a.n_heads, a.n_kv_heads, a.blocks_per_head, h, blk);
-    const int rpw = a.rows_per_wave;
-    const int RB = kWaves * rpw;
-    const int i0 = blk * RB;
-    const int nrows = min(RB, a.n_q - i0);
+    const int rpw = a.rows_per_wave, RB = NWG * rpw;
+    const int i0 = blk * RB + w * rpw;  // this wave's rows: i0 .. i0 + rpw - 1
+    const int nrows = max(0, min(rpw, a.n_q - i0));
     const int group = a.n_heads / a.n_kv_heads;
     const int c_sent = a.m + a.r, c_led = a.k + c_sent;
-    const int P = a.pieces;  // pieces per key per pass (power of two, divides DP)
-    const int npass = DP / P;
+    const int rounds = (c_led + 15) >> 4;
+    const unsigned char *Kg = reinterpret_cast<const unsigned char *>(a.K) + (int64_t)(h / group) * a.n_k * ROWB;
+    const unsigned char *Qb = reinterpret_cast<const unsigned char *>(a.Q);
     const int64_t row0 = (int64_t)h * a.n_q + i0;
 
-    u32x4_t *kb = reinterpret_cast<u32x4_t *>(smem);        // [n_k][P]
-    u32x4_t *qb = kb + (int64_t)a.n_k * P;                     // [RB][P]
-    const unsigned char *Kg = reinterpret_cast<const unsigned char *>(a.K) + (int64_t)(h / group) * a.n_k * ROWB;
-    const unsigned char *Qg = reinterpret_cast<const unsigned char *>(a.Q) + row0 * ROWB;
-
-    // slot ids of this wave's rows (local row w + kWaves * q), lane j <-> slot j + 64 e
-    int ids[RPW][E];
-    float acc[RPW][E];
-#pragma unroll
-    for (int q = 0; q < RPW; ++q) {
-        const int lr = w + kWaves * q;
+    auto load_ids = [&](int64_t row, int (&idr)[E]) {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
             const int slot = e * 64 + lane;
             int id = -1;
-            if (q < rpw && lr < nrows) {
-                const int64_t row = row0 + lr;
-                if (slot < a.k)
-                    id = a.led_routes[row * a.k + slot];
-                else if (slot < c_led)
-                    id = a.led_sent[row * c_sent + (slot - a.k)];
-            }
-            ids[q][e] = id;
-            acc[q][e] = 0.0f;
+            if (slot < a.k)
+                id = a.led_routes[row * a.k + slot];
+            else if (slot < c_led)
+                id = a.led_sent[row * c_sent + (slot - a.k)];
+            idr[e] = id;
         }
-    }
+    };
+    auto load_q = [&](int64_t row, u32x4_t (&qv)[CH]) {
+#pragma unroll
+        for (int c = 0; c < CH; ++c) qv[c] = *reinterpret_cast<const u32x4_t *>(Qb + row * ROWB + (c * 4 + pq) * 16);
+    };
 
-    for (int ps = 0; ps < npass; ++ps) {
-        if (ps > 0) __syncthreads();  // every wave is done with the previous slice
-        // stage slice ps of the key rows and of the block's query rows
-        const int nk = a.n_k * P, lp = __builtin_ctz(P);
-        for (int t0 = tid; t0 < nk; t0 += kStageUnroll * kThreads) {
-            u32x4_t v[kStageUnroll];
-#pragma unroll
-            for (int u = 0; u < kStageUnroll; ++u) {
-                const int t = min(t0 + u * kThreads, nk - 1);  // clamped: the loads carry no branch
-                const int key = t >> lp, pc = t & (P - 1);
-                v[u] = *reinterpret_cast<const u32x4_t *>(Kg + (int64_t)key * ROWB + (ps * P + pc) * 16);
-            }
-#pragma unroll
-            for (int u = 0; u < kStageUnroll; ++u)
-                if (t0 + u * kThreads < nk) kb[t0 + u * kThreads] = v[u];
-        }
-        for (int t = tid; t < nrows * P; t += kThreads) {
-            const int r = t >> lp, pc = t & (P - 1);
-            qb[t] = *reinterpret_cast<const u32x4_t *>(Qg + (int64_t)r * ROWB + (ps * P + pc) * 16);
-        }
-        __syncthreads();
-#pragma unroll
-        for (int q = 0; q < RPW; ++q) {
-            const int lr = w + kWaves * q;
-            if (q < rpw && lr < nrows) {
-                const u32x4_t *qr = qb + lr * P;
-#pragma unroll
-                for (int e = 0; e < E; ++e) {
-                    const int id = ids[q][e];
-                    if (id >= 0) {
-                        const u32x4_t *kr = kb + (int64_t)id * P;
-                        float s = acc[q][e];
-                        for (int u = 0; u < P; ++u) {
-                            const int pc = (u + lane) & (P - 1);
-                            s = dot16<DT>(qr[pc], kr[pc], s);
-                        }
-                        acc[q][e] = s;
-                    }
-                }
-            }
-        }
-    }
-    // per row: alpha, beta and the candidate counts by wave reductions; lane q
-    // keeps row q's values
     float my_a = INFINITY, my_b = -INFINITY;
     int my_nc = 0, my_ns = 0;
+    int idr[E];
+    u32x4_t qv[CH];
+    if (nrows > 0) {
+        load_ids(row0, idr);
+        load_q(row0, qv);
+    }
+    for (int q = 0; q < nrows; ++q) {
+        int idn[E];
+        u32x4_t qn[CH];
+        if (q + 1 < nrows) {
+            load_ids(row0 + q + 1, idn);
+            load_q(row0 + q + 1, qn);
+        }
+        int ids[NR];
+        u32x4_t kv[NR][CH];
 #pragma unroll
-    for (int q = 0; q < RPW; ++q) {
-        const int lr = w + kWaves * q;
-        if (q < rpw && lr < nrows) {
-            float amin = INFINITY, bmax = -INFINITY;
-            int nc = 0, ns = 0;
+        for (int u = 0; u < NR; ++u) {
+            const int slot = u * 16 + G;
+            ids[u] = (u < rounds) ? __shfl(idr[u >> 2], slot & 63, 64) : -1;
+            const unsigned char *kp = Kg + (int64_t)max(ids[u], 0) * ROWB;
 #pragma unroll
-            for (int e = 0; e < E; ++e) {
-                const int slot = e * 64 + lane;
-                const bool inR = ids[q][e] >= 0 && slot < a.k, inC = ids[q][e] >= 0 && slot >= a.k;
-                amin = inR ? fminf(amin, acc[q][e]) : amin;
-                bmax = inC ? fmaxf(bmax, acc[q][e]) : bmax;
-                nc += __popcll(__ballot(inR));
-                ns += __popcll(__ballot(inC));
-            }
+            for (int c = 0; c < CH; ++c) kv[u][c] = *reinterpret_cast<const u32x4_t *>(kp + (c * 4 + pq) * 16);
+        }
+        float amin = INFINITY, bmax = -INFINITY;
+        int nc = 0, ns = 0;
 #pragma unroll
-            for (int off = 32; off > 0; off >>= 1) {
-                amin = fminf(amin, __shfl_xor(amin, off, 64));
-                bmax = fmaxf(bmax, __shfl_xor(bmax, off, 64));
-            }
-            if (lane == q) {
-                my_a = amin;
-                my_b = bmax;
-                my_nc = nc;
-                my_ns = ns;
-            }
+        for (int u = 0; u < NR; ++u) {
+            const int slot = u * 16 + G;
+            float part = 0.0f;
+#pragma unroll
+            for (int c = 0; c < CH; ++c) part = dot16<DT>(qv[c], kv[u][c], part);
+            part = quad_sum(part);
+            const bool inR = ids[u] >= 0 && slot < a.k, inC = ids[u] >= 0 && slot >= a.k;
+            amin = inR ? fminf(amin, part) : amin;
+            bmax = inC ? fmaxf(bmax, part) : bmax;
+            nc += __popcll(__ballot(inR && pq == 0));
+            ns += __popcll(__ballot(inC && pq == 0));
+        }
+        amin = wave_extremum<true>(amin);
+        bmax = wave_extremum<false>(bmax);
+        if (lane == q) {
+            my_a = amin;
+            my_b = bmax;
+            my_nc = nc;
+            my_ns = ns;
+        }
+        if (q + 1 < nrows) {
+#pragma unroll
+            for (int e = 0; e < E; ++e) idr[e] = idn[e];
+#pragma unroll
+            for (int c = 0; c < CH; ++c) qv[c] = qn[c];
         }
     }
 
-    // one lane per row: the trigger, outputs, age, counts
     unsigned long long pairs_t = 0;
     unsigned cnt_t = 0;
-    {
-        const int lr = w + kWaves * lane;
-        if (lane < rpw && lr < nrows) {
-            const int i = i0 + lr;
-            const int64_t row = row0 + lr;
-            const bool flag = my_ns > 0 && (my_b + a.gamma >= my_a);
-            a.flags[row] = flag ? 1 : 0;
-            if (a.mask_out) a.mask_out[row] = flag ? 1 : 0;
-            a.alpha[row] = my_a;
-            a.beta[row] = my_b;
-            if (!flag) a.led_age[row] = a.layer - a.led_build[row];
-            const int ni = a.causal ? min(i + 1, a.n_k) : a.n_k;
-            pairs_t = (unsigned long long)(my_nc + my_ns + (flag ? ni : 0));
-            cnt_t = flag ? 1u : 0u;
-        }
+    if (lane < nrows) {
+        const int i = i0 + lane;
+        const int64_t row = row0 + lane;
+        const bool flag = my_ns > 0 && (my_b + a.gamma >= my_a);
+        a.flags[row] = flag ? 1 : 0;
+        if (a.mask_out) a.mask_out[row] = flag ? 1 : 0;
+        a.alpha[row] = my_a;
+        a.beta[row] = my_b;
+        if (!flag) a.led_age[row] = a.layer - a.led_build[row];
+        const int ni = a.causal ? min(i + 1, a.n_k) : a.n_k;
+        pairs_t = (unsigned long long)(my_nc + my_ns + (flag ? ni : 0));
+        cnt_t = flag ? 1u : 0u;
     }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
@@ -228,7 +220,7 @@ __global__ __launch_bounds__(kThreads) void rescore_kernel(RescoreArgs a)
         unsigned long long P2 = 0;
         unsigned C = 0;
 #pragma unroll
-        for (int v = 0; v < kWaves; ++v) {
+        for (int v = 0; v < NWG; ++v) {
             P2 += s_pairs[v];
             C += s_cnt[v];
         }
@@ -238,69 +230,50 @@ __global__ __launch_bounds__(kThreads) void rescore_kernel(RescoreArgs a)
     }
 }
 
-template <typename DT, int D, int E>
-hipError_t launch_e(const RescoreArgs &a, size_t lds, hipStream_t stream)
-{
-    const void *fn = reinterpret_cast<const void *>(&rescore_kernel<DT, D, E>);
-    if (lds > 65536) {
-        hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
-    }
-    const int grid = a.n_heads * a.blocks_per_head;
-    hipLaunchKernelGGL((rescore_kernel<DT, D, E>), dim3(grid), dim3(kThreads), lds, stream, a);
-    return hipGetLastError();
-}
-
 template <typename DT, int D>
-hipError_t launch_d(const RescoreArgs &a, size_t lds, hipStream_t stream)
+hipError_t launch_d(const RescoreArgs &a, hipStream_t stream)
 {
+    const int grid = a.n_heads * a.blocks_per_head;
     const int c = a.k + a.m + a.r;
-    if (c <= 64) return launch_e<DT, D, 1>(a, lds, stream);
-    if (c <= 128) return launch_e<DT, D, 2>(a, lds, stream);
-    return launch_e<DT, D, 4>(a, lds, stream);
+    if (c <= 64)
+        hipLaunchKernelGGL((rescore_kernel<DT, D, 1>), dim3(grid), dim3(kThreads), 0, stream, a);
+    else if (c <= 128)
+        hipLaunchKernelGGL((rescore_kernel<DT, D, 2>), dim3(grid), dim3(kThreads), 0, stream, a);
+    else
+        hipLaunchKernelGGL((rescore_kernel<DT, D, 4>), dim3(grid), dim3(kThreads), 0, stream, a);
+    return hipGetLastError();
 }
 
 }  // namespace
 
-void rescore_geometry(int dtype, int d, int n_k, int64_t rows, int c, int n_q, RescoreGeometry &g)
+void rescore_geometry(int64_t rows, int n_q, RescoreGeometry &g)
 {
-    const int e = (dtype == 0) ? 4 : 2;
-    const int dp = d * e / 16;
-    // pieces per key per pass: the largest power of two (dividing dp) whose
-    // key slice fits the staging budget; one piece at the longest key counts
-    int p = 1;
-    while (p * 2 <= dp && (int64_t)n_k * p * 2 * 16 <= kRescoreKeyBudget) p *= 2;
-    g.pieces = p;
-    const int groups = (c + 63) / 64;
-    const int E = groups <= 1 ? 1 : (groups <= 2 ? 2 : 4);
-    const int rpw_max = kRescoreSlotRows / E;
-    // rows per wave: enough workgroups to give every compute unit two
-    int64_t per = rows / (512 * kRescoreWaves);
+    // rows per wave: about kRescoreBlocks workgroups in all, never more rows
+    // per workgroup than a head has
+    int64_t per = rows / ((int64_t)kRescoreBlocks * kRescoreWaves);
     int rpw = 1;
-    while (rpw * 2 <= rpw_max && rpw * 2 <= per) rpw *= 2;
-    // a block never spans heads: no more rows than n_q (rounded to waves)
+    while (rpw * 2 <= kRescoreMaxRowsPerWave && rpw * 2 <= per) rpw *= 2;
     while (rpw > 1 && (int64_t)kRescoreWaves * (rpw / 2) >= n_q) rpw /= 2;
     g.rows_per_wave = rpw;
     g.rows_per_block = kRescoreWaves * rpw;
     g.blocks_per_head = (n_q + g.rows_per_block - 1) / g.rows_per_block;
-    g.lds_bytes = (size_t)n_k * p * 16 + (size_t)g.rows_per_block * p * 16;
 }
 
-hipError_t launch_rescore(const RescoreArgs &a, int dtype, size_t lds, hipStream_t stream)
+hipError_t launch_rescore(const RescoreArgs &a, int dtype, hipStream_t stream)
 {
     if (dtype == 0) {
         switch (a.d) {
-        case 32: return launch_d<float, 32>(a, lds, stream);
-        case 64: return launch_d<float, 64>(a, lds, stream);
-        case 128: return launch_d<float, 128>(a, lds, stream);
+        case 32: return launch_d<float, 32>(a, stream);
+        case 64: return launch_d<float, 64>(a, stream);
+        case 128: return launch_d<float, 128>(a, stream);
         default: break;
         }
     } else {
         switch (a.d) {
-        case 32: return launch_d<bf16_t, 32>(a, lds, stream);
-        case 64: return launch_d<bf16_t, 64>(a, lds, stream);
-        case 128: return launch_d<bf16_t, 128>(a, lds, stream);
-        case 256: return launch_d<bf16_t, 256>(a, lds, stream);
+        case 32: return launch_d<bf16_t, 32>(a, stream);
+        case 64: return launch_d<bf16_t, 64>(a, stream);
+        case 128: return launch_d<bf16_t, 128>(a, stream);
+        case 256: return launch_d<bf16_t, 256>(a, stream);
         default: break;
         }
     }
