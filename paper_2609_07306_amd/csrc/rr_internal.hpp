@@ -17,6 +17,7 @@ constexpr int kWideTileRows = 64;     // route tile rows when 64 < k + m <= 128
 constexpr int kRescoreWaves = 4;            // waves per rescoring workgroup
 constexpr int kRescoreBlocks = 512;         // target rescoring workgroups per launch (two per CU)
 constexpr int kRescoreMaxRowsPerWave = 16;  // rows a rescoring wave scores in turn
+constexpr int kRescoreLanesPerCand = 4;     // lanes sharing one candidate's dot product (4 or 8)
 
 struct RouteArgs {
     const void *Q;

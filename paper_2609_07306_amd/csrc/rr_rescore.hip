@@ -59,14 +59,16 @@ __device__ __forceinline__ float dot16<bf16_t>(const u32x4_t &q, const u32x4_t &
     return acc;
 }
 
-// Minimum / maximum over the 64 lanes of a wave, returned to every lane:
-// shifts within each row of 16 lanes, then row broadcasts carry rows 0..2
-// into lane 63, which is read back as a scalar.
-// Sum over the 4 lanes of a quad (DPP quad permutations, no LDS round trip).
-__device__ __forceinline__ float quad_sum(float x)
+// Sum over aligned groups of LPC lanes (4 or 8) with DPP permutations, no
+// LDS round trip: two quad permutations, then the half-row mirror, which
+// pairs each lane of one quad with a lane of the neighbouring quad.
+template <int LPC>
+__device__ __forceinline__ float group_sum(float x)
 {
     x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));  // lane ^ 1
     x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));  // lane ^ 2
+    if (LPC == 8)
+        x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x141, 0xF, 0xF, false));  // 7 - lane
     return x;
 }
 
@@ -76,6 +78,9 @@ __device__ __forceinline__ float dpp_move(float fill, float x)
     return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(fill), __float_as_int(x), CTRL, ROW_MASK, 0xF, false));
 }
 
+// Minimum / maximum over the 64 lanes of a wave, returned to every lane:
+// shifts within each row of 16 lanes, then row broadcasts carry rows 0..2
+// into lane 63, which is read back as a scalar.
 template <bool MIN>
 __device__ __forceinline__ float wave_extremum(float v)
 {
@@ -96,16 +101,18 @@ template <typename DT, int D, int E>
 __global__ __launch_bounds__(kThreads) void rescore_kernel(RescoreArgs a)
 {
     constexpr int ROWB = D * (int)sizeof(DT);
-    constexpr int CH = ROWB / 64;  // 16-byte pieces per lane (4 lanes per candidate)
-    static_assert(CH >= 1 && ROWB % 64 == 0, "row bytes must be a multiple of 64");
-    constexpr int NR = 4 * E;      // rounds of 16 candidates
+    constexpr int LPC = (ROWB >= 16 * kRescoreLanesPerCand) ? kRescoreLanesPerCand : 4;  // lanes per candidate
+    constexpr int CPR = 64 / LPC;         // candidates per round
+    constexpr int CH = ROWB / (16 * LPC);  // 16-byte pieces per lane
+    static_assert(CH >= 1 && ROWB % (16 * LPC) == 0, "row bytes must be a multiple of 16 lanes-per-candidate");
+    constexpr int NR = 64 * E / CPR;      // rounds
     constexpr int NWG = kRescoreWaves;
 
     __shared__ unsigned long long s_pairs[NWG];
     __shared__ unsigned s_cnt[NWG];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int G = lane >> 2, pq = lane & 3;
+    const int G = lane / LPC, pq = lane % LPC;
     int h, blk;
     tile_of_block(blockIdx.x, a.n_heads, a.n_kv_heads, a.blocks_per_head, h, blk);
     const int rpw = a.rows_per_wave, RB = NWG * rpw;
@@ -113,7 +120,7 @@ __global__ __launch_bounds__(kThreads) void rescore_kernel(RescoreArgs a)
     const int nrows = max(0, min(rpw, a.n_q - i0));
     const int group = a.n_heads / a.n_kv_heads;
     const int c_sent = a.m + a.r, c_led = a.k + c_sent;
-    const int rounds = (c_led + 15) >> 4;
+    const int rounds = (c_led + CPR - 1) / CPR;
     const unsigned char *Kg = reinterpret_cast<const unsigned char *>(a.K) + (int64_t)(h / group) * a.n_k * ROWB;
     const unsigned char *Qb = reinterpret_cast<const unsigned char *>(a.Q);
     const int64_t row0 = (int64_t)h * a.n_q + i0;
@@ -132,7 +139,7 @@ __global__ __launch_bounds__(kThreads) void rescore_kernel(RescoreArgs a)
     };
     auto load_q = [&](int64_t row, u32x4_t (&qv)[CH]) {
 #pragma unroll
-        for (int c = 0; c < CH; ++c) qv[c] = *reinterpret_cast<const u32x4_t *>(Qb + row * ROWB + (c * 4 + pq) * 16);
+        for (int c = 0; c < CH; ++c) qv[c] = *reinterpret_cast<const u32x4_t *>(Qb + row * ROWB + (c * LPC + pq) * 16);
     };
 
     float my_a = INFINITY, my_b = -INFINITY;
@@ -154,21 +161,24 @@ __global__ __launch_bounds__(kThreads) void rescore_kernel(RescoreArgs a)
         u32x4_t kv[NR][CH];
 #pragma unroll
         for (int u = 0; u < NR; ++u) {
-            const int slot = u * 16 + G;
-            ids[u] = (u < rounds) ? __shfl(idr[u >> 2], slot & 63, 64) : -1;
-            const unsigned char *kp = Kg + (int64_t)max(ids[u], 0) * ROWB;
+            const int slot = u * CPR + G;
+            ids[u] = -1;
+            if (u < rounds) {  // wave-uniform: rounds past the ledger width load nothing
+                ids[u] = __shfl(idr[(u * CPR) >> 6], slot & 63, 64);
+                const unsigned char *kp = Kg + (int64_t)max(ids[u], 0) * ROWB;
 #pragma unroll
-            for (int c = 0; c < CH; ++c) kv[u][c] = *reinterpret_cast<const u32x4_t *>(kp + (c * 4 + pq) * 16);
+                for (int c = 0; c < CH; ++c) kv[u][c] = *reinterpret_cast<const u32x4_t *>(kp + (c * LPC + pq) * 16);
+            }
         }
         float amin = INFINITY, bmax = -INFINITY;
         int nc = 0, ns = 0;
 #pragma unroll
         for (int u = 0; u < NR; ++u) {
-            const int slot = u * 16 + G;
+            const int slot = u * CPR + G;
             float part = 0.0f;
 #pragma unroll
             for (int c = 0; c < CH; ++c) part = dot16<DT>(qv[c], kv[u][c], part);
-            part = quad_sum(part);
+            part = group_sum<LPC>(part);
             const bool inR = ids[u] >= 0 && slot < a.k, inC = ids[u] >= 0 && slot >= a.k;
             amin = inR ? fminf(amin, part) : amin;
             bmax = inC ? fmaxf(bmax, part) : bmax;
