@@ -18,6 +18,8 @@ constexpr int kRescoreWaves = 4;            // waves per rescoring workgroup
 constexpr int kRescoreBlocks = 512;         // target rescoring workgroups per launch (two per CU)
 constexpr int kRescoreMaxRowsPerWave = 16;  // rows a rescoring wave scores in turn
 constexpr int kRescoreLanesPerCand = 4;     // lanes sharing one candidate's dot product (4 or 8)
+constexpr int kRescoreDenseMaxKeys = 2048;  // dense (MFMA tile) rescoring up to this many key chunks
+constexpr int kRescoreDenseMinTiles = 256;  // ... and with at least this many 128-row tiles (one per CU)
 
 struct RouteArgs {
     const void *Q;
@@ -57,7 +59,9 @@ struct RescoreArgs {
     int32_t causal;
     int32_t layer;
     int32_t blocks_per_head;  // ceil(n_q / rows per block)
-    int32_t rows_per_wave;    // rows per block = kRescoreWaves * rows_per_wave
+    int32_t rows_per_wave;    // gather: rows per block = kRescoreWaves * rows_per_wave
+    int32_t dense;            // 1: the MFMA tile kernel (128-row tiles), 0: the gather kernel
+    int32_t bm_words;         // dense: bitmap words per row (covers the padded key range)
     float gamma;
     const int32_t *led_routes;
     const int32_t *led_sent;
@@ -78,8 +82,12 @@ hipError_t launch_route(const RouteArgs &a, int dtype, int grid, hipStream_t str
 // Launch shape of the rescoring kernel for a configuration.
 struct RescoreGeometry {
     int rows_per_wave, rows_per_block, blocks_per_head;
+    bool dense;
+    int bm_words;
 };
-void rescore_geometry(int64_t rows, int n_q, RescoreGeometry &g);
+void rescore_geometry(int64_t rows, int n_q, int n_k, RescoreGeometry &g);
 hipError_t launch_rescore(const RescoreArgs &a, int dtype, hipStream_t stream);
+int rescore_dense_tile_rows();
+hipError_t launch_rescore_dense(const RescoreArgs &a, int dtype, hipStream_t stream);
 
 }  // namespace rr

@@ -256,8 +256,22 @@ hipError_t launch_d(const RescoreArgs &a, hipStream_t stream)
 
 }  // namespace
 
-void rescore_geometry(int64_t rows, int n_q, RescoreGeometry &g)
+void rescore_geometry(int64_t rows, int n_q, int n_k, RescoreGeometry &g)
 {
+    // dense tiles when the key range is short enough for the bitmaps and the
+    // tiles fill the chip; otherwise the gather kernel
+    const int64_t tiles = (rows / n_q) * ((n_q + rescore_dense_tile_rows() - 1) / rescore_dense_tile_rows());
+    g.dense = n_k <= kRescoreDenseMaxKeys && tiles >= kRescoreDenseMinTiles;
+    if (g.dense) {
+        // 128-row tiles over the whole key range; two bitmap words per 64
+        // keys of the padded range
+        g.rows_per_wave = 0;
+        g.rows_per_block = rescore_dense_tile_rows();
+        g.blocks_per_head = (n_q + g.rows_per_block - 1) / g.rows_per_block;
+        g.bm_words = 2 * ((n_k + 63) / 64);
+        return;
+    }
+    g.bm_words = 0;
     // rows per wave: about kRescoreBlocks workgroups in all, never more rows
     // per workgroup than a head has
     int64_t per = rows / ((int64_t)kRescoreBlocks * kRescoreWaves);
@@ -271,6 +285,7 @@ void rescore_geometry(int64_t rows, int n_q, RescoreGeometry &g)
 
 hipError_t launch_rescore(const RescoreArgs &a, int dtype, hipStream_t stream)
 {
+    if (a.dense) return launch_rescore_dense(a, dtype, stream);
     if (dtype == 0) {
         switch (a.d) {
         case 32: return launch_d<float, 32>(a, stream);

@@ -1,0 +1,263 @@
+// Dense candidate rescoring for key heads of up to 2048 chunks (RouteRelay,
+// arXiv 2609.07306, Sec. 3.2 Eq. (5)-(8); Sec. 4.1-4.2).
+//
+// The sampled product of Eq. (5) names at most k + m + r keys per row, but
+// with n_k <= 2048 the candidates cover a few percent of a head's keys, and
+// on matrix cores the full product of a 128-row tile with all of its head's
+// keys costs less than gathering the candidate key rows one by one: the key
+// head streams once per tile through LDS (the routing sweep's staging), the
+// MFMAs produce every score, and the epilogue keeps a score only where the
+// row's ledger names the key.  Each row's ledger is turned into two bitmaps
+// over the key range (routed set R, candidate set C = near-miss + random
+// sentinels); per stage a lane reads the words of its 16 keys and folds
+//   alpha = min over R,  beta = max over C
+// with bit-select (a masked-out score becomes +inf for the minimum, -inf for
+// the maximum).  The scores are the ones the routing kernel computes (same
+// fragments, same MFMA order), so a route's score at rescoring is bitwise the
+// routing score when Q and K are unchanged.
+//
+// Row outputs and the per-workgroup tables match the gather kernel's: the
+// refresh flag (C non-empty and beta + gamma >= alpha), mask, alpha, beta,
+// the age of rows that keep their route, and per-tile flagged-row and
+// score-pair counts (score pairs follow the method's accounting: the ledger's
+// candidates, plus n_i for each refreshed row).
+
+#include "rr_route_impl.hpp"
+
+namespace rr {
+namespace {
+
+using route_detail::RT;
+
+// Tiles of 32 * kDenseRowBlocks rows; waves = row blocks x 2 key splits.
+constexpr int kDenseRowBlocks = 4;
+constexpr int kDenseThreads = 64 * kDenseRowBlocks * 2;
+template <typename DT, int D>
+using DenseRT = RT<DT, D, kDenseRowBlocks, 2, 2, 64, 32>;
+
+struct DenseEpi {
+    float amin, bmax;
+    int sbase;         // first key of the lane's segment
+    const uint2 *bmr;  // this lane's row: (R word, C word) per 32 keys
+
+    template <class F>
+    __device__ __forceinline__ void step(int st, const f32x16_t &acc, f32x16_t &next, const F &fq, const F &fk, bool)
+    {
+        const int k0 = sbase + 16 * st;  // this lane's keys: k0 .. k0 + 15 (k0 % 16 == 0)
+        const uint2 wv = bmr[k0 >> 5];
+        next = route_detail::tile_product(fq, fk);
+        const uint32_t sh = (uint32_t)(k0 & 16);
+        const uint32_t mr = wv.x >> sh, mc = wv.y >> sh;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const uint32_t xb = __float_as_uint(acc[i]);
+            // all-ones where key k0 + i is in the set, else zero
+            const uint32_t nr = (uint32_t)((int32_t)(mr << (31 - i)) >> 31);
+            const uint32_t nc = (uint32_t)((int32_t)(mc << (31 - i)) >> 31);
+            amin = fminf(amin, __uint_as_float((xb & nr) | (0x7F800000u & ~nr)));  // +inf when out
+            bmax = fmaxf(bmax, __uint_as_float((xb & nc) | (0xFF800000u & ~nc)));  // -inf when out
+        }
+        route_detail::interleave_mfma<F::NS, (16 * 6 + F::NS - 1) / F::NS>();
+    }
+};
+
+template <typename DT, int D>
+__global__ __launch_bounds__(kDenseThreads) void rescore_dense_kernel(RescoreArgs a)
+{
+    using C = DenseRT<DT, D>;
+    static_assert(C::NT == kDenseThreads, "launch bounds of the tile shape");
+    constexpr int BM = C::BM, NT = C::NT, NW = kDenseRowBlocks, KS = 2;
+    constexpr int NWB = (BM + 63) / 64;  // waves holding one lane per row
+    extern __shared__ __align__(16) unsigned char smem[];
+    unsigned char *bt = smem;                                     // [2][KS][32][BSTR] key tiles
+    uint2 *bm = reinterpret_cast<uint2 *>(smem + 2 * C::ST);      // [BM][bm_words]
+    __shared__ int32_t row_n[BM], s_nc[BM], s_ns[BM];
+    __shared__ float s_amin[KS][BM], s_bmax[KS][BM];
+    __shared__ unsigned long long s_pairs[NWB];
+    __shared__ unsigned s_cnt[NWB];
+
+    const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
+    const int rb = w % NW, p = w / NW;
+    const int nwd = a.bm_words;
+    int h, t;
+    tile_of_block(blockIdx.x, a.n_heads, a.n_kv_heads, a.blocks_per_head, h, t);
+    const int i0 = t * BM;
+    const int64_t g0 = (int64_t)h * a.n_q + i0;  // first row of the tile
+    const int c_sent = a.m + a.r, c_led = a.k + c_sent;
+
+    // the query fragments are requested first: their latency overlaps the
+    // bitmap set-up
+    const int myrow = 32 * rb + l32;
+    Frag<DT, D> fq;
+    if (i0 + myrow < a.n_q)
+        fq.load(reinterpret_cast<const DT *>(a.Q) + (g0 + myrow) * D, hh);
+    else
+        fq.zero();
+
+    // ledger rows -> bitmaps.  Wave w takes rows w, w + 8, ... (RPW rows),
+    // lane = slot.  Every lane loads (rows past n_q and slots past the ledger
+    // read the tile's first row and are masked), so the loads carry no
+    // branches; the first chunk's loads are issued before the bitmaps are
+    // cleared, and the set-up barriers order LDS only, so the query, ledger
+    // and first key loads are all in flight together.  The counts are of the
+    // ledger's filled slots.
+    constexpr int RPW = BM / C::NWV;
+    auto load_chunk = [&](int s0, int (&id)[RPW]) {
+        const int slot = s0 + lane;
+        const bool inr = slot < a.k, live = slot < c_led;
+#pragma unroll
+        for (int q = 0; q < RPW; ++q) {
+            const int r = w + q * C::NWV;
+            const int64_t row = (i0 + r < a.n_q) ? g0 + r : g0;
+            const int32_t *src = inr ? a.led_routes + row * a.k + slot
+                                     : (live ? a.led_sent + row * c_sent + (slot - a.k) : a.led_routes + g0 * a.k);
+            id[q] = (i0 + r < a.n_q && live) ? *src : -1;
+        }
+    };
+    int id[RPW];
+    load_chunk(0, id);
+
+    for (int j = tid; j < BM * nwd; j += NT) bm[j] = make_uint2(0u, 0u);
+    if (tid < BM) {
+        const int i = i0 + tid;
+        row_n[tid] = (i < a.n_q) ? (a.causal ? min(i + 1, a.n_k) : a.n_k) : 0;
+    }
+    lds_barrier();
+
+    int nc[RPW], ns[RPW];
+#pragma unroll
+    for (int q = 0; q < RPW; ++q) nc[q] = ns[q] = 0;
+    uint32_t *bw = reinterpret_cast<uint32_t *>(bm);
+    for (int s0 = 0; s0 < c_led; s0 += 64) {
+        if (s0 > 0) load_chunk(s0, id);
+        const bool inr = s0 + lane < a.k;
+#pragma unroll
+        for (int q = 0; q < RPW; ++q) {
+            const int r = w + q * C::NWV;
+            const bool ok = id[q] >= 0 && id[q] < a.n_k;  // ledger ids lie in [0, n_i); -1 is an empty slot
+            // word (id >> 5) of the row: .x holds R, .y holds C
+            if (ok) atomicOr(&bw[2 * (r * nwd + (id[q] >> 5)) + (inr ? 0 : 1)], 1u << (id[q] & 31));
+            nc[q] += __popcll(__ballot(ok && inr));
+            ns[q] += __popcll(__ballot(ok && !inr));
+        }
+    }
+    if (lane == 0) {
+#pragma unroll
+        for (int q = 0; q < RPW; ++q) {
+            const int r = w + q * C::NWV;
+            s_nc[r] = nc[q];
+            s_ns[r] = ns[q];
+        }
+    }
+    lds_barrier();
+    // the tile's longest valid key range (tiles always hold a row)
+    const int ncols = a.causal ? min(min(i0 + BM, a.n_q), a.n_k) : a.n_k;
+    const int nb = __builtin_amdgcn_readfirstlane((ncols + 32 * KS - 1) / (32 * KS));
+    const int seg = 16 * nb;
+
+    const int myseg = 2 * p + hh;
+    const unsigned char *Kg = reinterpret_cast<const unsigned char *>(a.K) +
+                              (int64_t)(h / (a.n_heads / a.n_kv_heads)) * a.n_k * C::ROWB;
+    DenseEpi epi;
+    epi.amin = INFINITY;
+    epi.bmax = -INFINITY;
+    epi.sbase = myseg * seg;
+    epi.bmr = bm + myrow * nwd;
+    // double-buffered key fragments where a second set fits in registers
+    if constexpr (sizeof(DT) * D <= 256)
+        route_detail::sweep_keys_db<DT, D, C>(fq, Kg, a.n_k, seg, nb, nb, tid, p, hh, l32, bt, epi);
+    else
+        route_detail::sweep_keys<DT, D, C>(fq, Kg, a.n_k, seg, nb, nb, tid, p, hh, l32, bt, epi);
+
+    // the row's four lanes: halves hh of a wave, then the key splits p
+    float amin = fminf(epi.amin, __shfl_xor(epi.amin, 32, 64));
+    float bmax = fmaxf(epi.bmax, __shfl_xor(epi.bmax, 32, 64));
+    if (hh == 0) {
+        s_amin[p][myrow] = amin;
+        s_bmax[p][myrow] = bmax;
+    }
+    __syncthreads();
+
+    unsigned long long pairs_t = 0;
+    unsigned cnt_t = 0;
+    if (tid < BM && i0 + tid < a.n_q) {
+        const int64_t row = g0 + tid;
+        const float al = fminf(s_amin[0][tid], s_amin[1][tid]);
+        const float be = fmaxf(s_bmax[0][tid], s_bmax[1][tid]);
+        const int nc = s_nc[tid], ns = s_ns[tid];
+        const bool flag = ns > 0 && (be + a.gamma >= al);
+        a.flags[row] = flag ? 1 : 0;
+        if (a.mask_out) a.mask_out[row] = flag ? 1 : 0;
+        a.alpha[row] = al;
+        a.beta[row] = be;
+        if (!flag) a.led_age[row] = a.layer - a.led_build[row];
+        pairs_t = (unsigned long long)(nc + ns + (flag ? row_n[tid] : 0));
+        cnt_t = flag ? 1u : 0u;
+    }
+    if (tid < 64 * NWB) {
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+            pairs_t += (unsigned long long)__shfl_xor((long long)pairs_t, off, 64);
+            cnt_t += (unsigned)__shfl_xor((int)cnt_t, off, 64);
+        }
+        if (lane == 0) {
+            s_pairs[w] = pairs_t;
+            s_cnt[w] = cnt_t;
+        }
+    }
+    __syncthreads();
+    if (tid == 0) {
+        const int slot = h * a.blocks_per_head + t;  // head-major
+        unsigned long long P2 = 0;
+        unsigned Cn = 0;
+#pragma unroll
+        for (int v = 0; v < NWB; ++v) {
+            P2 += s_pairs[v];
+            Cn += s_cnt[v];
+        }
+        a.blk_pairs[slot] = (int64_t)P2;
+        a.blk_count[slot] = (int32_t)Cn;
+    }
+}
+
+template <typename DT, int D>
+hipError_t launch_d(const RescoreArgs &a, hipStream_t stream)
+{
+    using C = DenseRT<DT, D>;
+    const size_t lds = (size_t)2 * C::ST + (size_t)C::BM * a.bm_words * sizeof(uint2);
+    const void *fn = reinterpret_cast<const void *>(&rescore_dense_kernel<DT, D>);
+    if (lds > 65536) {
+        const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL((rescore_dense_kernel<DT, D>), dim3(a.n_heads * a.blocks_per_head), dim3(C::NT), lds, stream,
+                       a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+int rescore_dense_tile_rows() { return DenseRT<float, 32>::BM; }
+
+hipError_t launch_rescore_dense(const RescoreArgs &a, int dtype, hipStream_t stream)
+{
+    if (dtype == 0) {
+        switch (a.d) {
+        case 32: return launch_d<float, 32>(a, stream);
+        case 64: return launch_d<float, 64>(a, stream);
+        case 128: return launch_d<float, 128>(a, stream);
+        default: break;
+        }
+    } else {
+        switch (a.d) {
+        case 32: return launch_d<bf16_t, 32>(a, stream);
+        case 64: return launch_d<bf16_t, 64>(a, stream);
+        case 128: return launch_d<bf16_t, 128>(a, stream);
+        case 256: return launch_d<bf16_t, 256>(a, stream);
+        default: break;
+        }
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace rr
