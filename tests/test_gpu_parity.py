@@ -219,6 +219,9 @@ ROLLOUTS = [
               "causal": True, "dtype": "bf16"}),
     ("tiny", {"m": 0, "r": 6, "n_layers": 4}),
     ("tiny", {"m": 6, "r": 0, "n_layers": 4}),
+    # enough 128-row tiles (one per compute unit) for the dense MFMA rescoring
+    ("scale", {"n_heads": 256, "n_kv_heads": 256, "n": 128, "n_layers": 6}),
+    ("gqa", {"n_heads": 256, "n_kv_heads": 64, "n": 128, "n_layers": 6}),
 ]
 
 
@@ -283,7 +286,7 @@ FULL_SIZE = [
 def test_full_size_sampled(name, kw):
     """At the workload's real size, in the launch configuration the benchmark
     uses: an anchor, then a relay in step mode, checked on sampled rows."""
-    from parity_util import dev, ledger_np, problem_of, route_ties, trigger_ties
+    from parity_util import dev, ledger_np, problem_of, route_ties, trigger_ties, TOL
     rr = rrmod()
     w = synth.preset(name, n_layers=2, **kw)
     note(f"full-size sampled: {w.name} n={w.n} heads={w.n_heads}")
@@ -320,6 +323,16 @@ def test_full_size_sampled(name, kw):
     same = dec & ~(om.astype(bool) & (t1b | t2b))
     for key in ("routes", "sent", "build", "age"):
         np.testing.assert_array_equal(got1[key][rows[same]], led[key][rows[same]])
+    # alpha and beta of the sampled rows against the oracle's binary64 scores
+    alpha, beta, _ = L.relay_stats()
+    torch.cuda.synchronize()
+    alpha, beta = alpha.cpu().numpy()[rows], beta.cpu().numpy()[rows]
+    tol = TOL[w.dtype]
+    oa, ob = out["alpha"][rows], out["beta"][rows]
+    fa, fb = np.isfinite(oa), np.isfinite(ob)
+    assert np.all(np.abs(alpha[fa] - oa[fa]) <= tol * out["alpha_abs"][rows][fa] + 1e-30)
+    assert np.all(np.abs(beta[fb] - ob[fb]) <= tol * out["beta_abs"][rows][fb] + 1e-30)
+    assert np.array_equal(np.isposinf(alpha), np.isposinf(oa)) and np.array_equal(np.isneginf(beta), np.isneginf(ob))
     cand = (got0["routes"] >= 0).sum(1) + (got0["sent"] >= 0).sum(1)
     ni = np.minimum(np.arange(p.rows) % p.n_q + 1, p.n_k) if p.causal else np.full(p.rows, p.n_k)
     assert int(pairs.item()) == int(cand.sum() + ni[gm.astype(bool)].sum())
