@@ -236,7 +236,7 @@ def main():
     mpeak = PEAK["mfma_bf16"] if w.dtype == "bf16" else PEAK["mfma_f32"]
     alg = {
         # per launch: (bound, algorithmic amount, unit, peak)
-        "rescore": ("hbm", (rows * (c * 4 + w.d * e_bytes + 22) + kvb) / 1e9, "GB/s", PEAK["hbm"]),
+        "rescore": ("hbm", (rows * (c * 4 + w.d * e_bytes + 18) + kvb) / 1e9, "GB/s", PEAK["hbm"]),
         "anchor": ("mfma", 2.0 * w.d * full_pairs_layer / 1e12, "TFLOP/s", mpeak),
         "reroute": ("mfma", 2.0 * w.d * mean_rerouted * mean_ni / 1e12, "TFLOP/s", mpeak),
         "full": ("mfma", 2.0 * w.d * full_pairs_layer / 1e12, "TFLOP/s", mpeak),

@@ -168,7 +168,7 @@ typedef enum {
     RR_KERNEL_FULL = 0,     /* GEMM + TopK, full routing */
     RR_KERNEL_ANCHOR = 1,   /* GEMM + TopK + ledger build, every row */
     RR_KERNEL_REROUTE = 2,  /* GEMM + TopK + ledger build, compacted rows */
-    RR_KERNEL_RESCORE = 3,  /* gather-dot, trigger, compaction counts, ages */
+    RR_KERNEL_RESCORE = 3,  /* rescoring (dense tiles or gather), trigger, compaction counts, ages */
     RR_KERNEL_KINDS = 4
 } rr_kernel_kind;
 
