@@ -37,11 +37,16 @@
  *   - trigger: a row is rerouted iff C is non-empty and beta + gamma >= alpha
  *     (the negation of the reuse test; equality reroutes);
  *   - random probes use the splitmix64 output function chained over
- *     (seed, layer, row, slot, attempt), reduced modulo n_i; up to 64
- *     attempts per slot reject ids outside the pool or already drawn; after
- *     that the slot takes the y-th remaining pool id in ascending order with
- *     y = probe(attempt 64) mod (remaining pool size); a pool no larger than
- *     r is taken whole in ascending order;
+ *     (seed, layer, row, slot, attempt); a pool no larger than r is taken
+ *     whole in ascending order; a pool of at most half the valid chunks is
+ *     sampled by rank: slot s takes the y-th remaining pool id in ascending
+ *     order with y = probe(attempt 0) mod (pool size - s); a larger pool by
+ *     rejection: probes reduced modulo n_i, up to 64 attempts per slot
+ *     rejecting ids outside the pool or already drawn, after which the slot
+ *     takes the y-th remaining pool id with y = probe(attempt 64) mod
+ *     (remaining pool size).  Both are uniform draws without replacement
+ *     (Eq. (10)); rank sampling spares the small pools of early causal rows
+ *     their long rejection runs;
  *   - random sentinels persist until the row is next rebuilt;
  *   - score pairs: a (re)built row counts its n_i scores, a relay row counts
  *     |A| (valid candidate slots) plus n_i when it is rerouted;
@@ -208,6 +213,22 @@ static void draw_random(const orc_problem *P, int32_t layer, int64_t row, int ni
         for (int j = 0; j < ni; ++j)
             if (!excl[j]) out[w++] = j;
         for (; w < r; ++w) out[w] = -1;
+        return;
+    }
+    if (2 * pool <= ni) {
+        /* rank sampling: the y-th remaining pool id, ascending */
+        for (int s = 0; s < r; ++s) {
+            uint64_t h = orc_probe_hash(P->seed, (uint64_t)layer, (uint64_t)row, (uint64_t)s, 0);
+            int y = (int)(h % (uint64_t)(pool - s));
+            int chosen = -1;
+            for (int j = 0; j < ni; ++j) {
+                if (excl[j]) continue;
+                if (y == 0) { chosen = j; break; }
+                --y;
+            }
+            excl[chosen] = 1;
+            out[s] = chosen;
+        }
         return;
     }
     for (int s = 0; s < r; ++s) {

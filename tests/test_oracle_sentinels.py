@@ -81,9 +81,48 @@ def test_uniform_over_pool_chi_square():
     assert chi1.pvalue > 1e-4, chi1
 
 
-def test_fallback_path_uniform():
-    """A pool of 10 among 1000 valid chunks makes most slots exhaust the 64
-    rejection attempts; the rank fallback keeps the draw uniform and distinct."""
+def _draw_by_definition(p, layer, row, ni, R, N):
+    """The sampling rule restated from the hash alone (the probe hash is pinned
+    to the published splitmix64 outputs above)."""
+    pool = [j for j in range(ni) if j not in set(R) | set(N)]
+    if len(pool) <= p.r:
+        return pool + [-1] * (p.r - len(pool))
+    out = []
+    rem = list(pool)
+    for s in range(p.r):
+        if 2 * len(pool) <= ni:
+            y = oracle.probe_hash(p.seed, layer, row, s, 0) % (len(pool) - s)
+            x = rem[y]
+        else:
+            x = None
+            for t in range(64):
+                cand = oracle.probe_hash(p.seed, layer, row, s, t) % ni
+                if cand in rem:
+                    x = cand
+                    break
+            if x is None:
+                x = rem[oracle.probe_hash(p.seed, layer, row, s, 64) % len(rem)]
+        rem.remove(x)
+        out.append(x)
+    return out
+
+
+@pytest.mark.parametrize("ni,nR,nN", [(100, 10, 5), (64, 20, 12), (40, 12, 8), (200, 60, 45), (33, 8, 8)])
+def test_draw_matches_definition(ni, nR, nN):
+    """Both regimes (rank sampling for pools of at most half the valid chunks,
+    rejection otherwise), slot by slot, on many rows."""
+    p = Problem(1, 1, 1, ni, 4, k=nR, m=nN, r=9, seed=77)
+    rng = np.random.default_rng(ni)
+    for row in range(60):
+        perm = rng.permutation(ni)
+        R, N = sorted(perm[:nR].tolist()), sorted(perm[nR:nR + nN].tolist())
+        want = _draw_by_definition(p, 5, row, ni, R, N)
+        np.testing.assert_array_equal(_draw(p, 5, row, ni, R, N), want)
+
+
+def test_rank_regime_uniform():
+    """A pool of 10 among 1000 valid chunks is sampled by rank; the draw is
+    uniform over the pool and without replacement."""
     p = Problem(1, 1, 1, 1000, 4, k=500, m=490, r=4, seed=5)
     R = list(range(0, 1000, 2))
     N = [j for j in range(1, 1000, 2)][:490]
