@@ -219,9 +219,15 @@ ROLLOUTS = [
               "causal": True, "dtype": "bf16"}),
     ("tiny", {"m": 0, "r": 6, "n_layers": 4}),
     ("tiny", {"m": 6, "r": 0, "n_layers": 4}),
-    # enough 128-row tiles (one per compute unit) for the dense MFMA rescoring
+    # enough 128-row tiles (one per compute unit) for the dense MFMA rescoring,
+    # for each input type and d (d = 256 bf16 takes the single-buffered sweep)
     ("scale", {"n_heads": 256, "n_kv_heads": 256, "n": 128, "n_layers": 6}),
     ("gqa", {"n_heads": 256, "n_kv_heads": 64, "n": 128, "n_layers": 6}),
+    ("drift", {"n_heads": 256, "n_kv_heads": 256, "n": 128, "n_layers": 4, "anchor_every": 2}),
+    ("drift", {"n_heads": 256, "n_kv_heads": 128, "n": 160, "d": 32, "n_layers": 4, "anchor_every": 2,
+               "causal": True}),
+    ("scale", {"n_heads": 256, "n_kv_heads": 256, "n": 128, "d": 64, "n_layers": 4, "anchor_every": 2}),
+    ("scale", {"n_heads": 256, "n_kv_heads": 256, "n": 128, "d": 256, "n_layers": 4, "anchor_every": 2}),
 ]
 
 
