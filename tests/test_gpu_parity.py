@@ -228,6 +228,12 @@ ROLLOUTS = [
                "causal": True}),
     ("scale", {"n_heads": 256, "n_kv_heads": 256, "n": 128, "d": 64, "n_layers": 4, "anchor_every": 2}),
     ("scale", {"n_heads": 256, "n_kv_heads": 256, "n": 128, "d": 256, "n_layers": 4, "anchor_every": 2}),
+    # dense rescoring with no near-miss slots, with no random slots, and with
+    # the wide route class (k + m > 64, 64-row route tiles)
+    ("scale", {"n_heads": 256, "n_kv_heads": 256, "n": 128, "m": 0, "n_layers": 4, "anchor_every": 2}),
+    ("scale", {"n_heads": 256, "n_kv_heads": 256, "n": 128, "r": 0, "n_layers": 4, "anchor_every": 2}),
+    ("scale", {"n_heads": 256, "n_kv_heads": 256, "n": 192, "k": 48, "m": 24, "r": 8, "n_layers": 4,
+               "anchor_every": 2}),
 ]
 
 
