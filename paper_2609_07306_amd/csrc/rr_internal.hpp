@@ -61,7 +61,7 @@ struct RescoreArgs {
     int32_t blocks_per_head;  // ceil(n_q / rows per block)
     int32_t rows_per_wave;    // gather: rows per block = kRescoreWaves * rows_per_wave
     int32_t dense;            // 1: the MFMA tile kernel (128-row tiles), 0: the gather kernel
-    int32_t bm_words;         // dense: bitmap words per row (covers the padded key range)
+    int32_t bm_words;         // dense: bitmap row stride in (R, C) word pairs (padded key range + 1, odd)
     float gamma;
     const int32_t *led_routes;
     const int32_t *led_sent;

@@ -263,12 +263,14 @@ void rescore_geometry(int64_t rows, int n_q, int n_k, RescoreGeometry &g)
     const int64_t tiles = (rows / n_q) * ((n_q + rescore_dense_tile_rows() - 1) / rescore_dense_tile_rows());
     g.dense = n_k <= kRescoreDenseMaxKeys && tiles >= kRescoreDenseMinTiles;
     if (g.dense) {
-        // 128-row tiles over the whole key range; two bitmap words per 64
-        // keys of the padded range
+        // 128-row tiles over the whole key range; a bitmap row holds two
+        // word pairs per 64 keys of the padded range plus one, so that rows
+        // lie an odd number of pairs apart and the 32 rows a wave reads
+        // together fall in distinct LDS banks
         g.rows_per_wave = 0;
         g.rows_per_block = rescore_dense_tile_rows();
         g.blocks_per_head = (n_q + g.rows_per_block - 1) / g.rows_per_block;
-        g.bm_words = 2 * ((n_k + 63) / 64);
+        g.bm_words = 2 * ((n_k + 63) / 64) + 1;
         return;
     }
     g.bm_words = 0;

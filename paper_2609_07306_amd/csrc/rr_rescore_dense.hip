@@ -70,7 +70,7 @@ __global__ __launch_bounds__(kDenseThreads) void rescore_dense_kernel(RescoreArg
     constexpr int NWB = (BM + 63) / 64;  // waves holding one lane per row
     extern __shared__ __align__(16) unsigned char smem[];
     unsigned char *bt = smem;                                     // [2][KS][32][BSTR] key tiles
-    uint2 *bm = reinterpret_cast<uint2 *>(smem + 2 * C::ST);      // [BM][bm_words]
+    uint2 *bm = reinterpret_cast<uint2 *>(smem + 2 * C::ST);      // [BM][bm_words] (R word, C word) pairs
     __shared__ int32_t row_n[BM], s_nc[BM], s_ns[BM];
     __shared__ float s_amin[KS][BM], s_bmax[KS][BM];
     __shared__ unsigned long long s_pairs[NWB];
