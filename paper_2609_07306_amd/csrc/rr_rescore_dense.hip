@@ -98,9 +98,9 @@ __global__ __launch_bounds__(kDenseThreads) void rescore_dense_kernel(RescoreArg
     // lane = slot.  Every lane loads (rows past n_q and slots past the ledger
     // read the tile's first row and are masked), so the loads carry no
     // branches; the first chunk's loads are issued before the bitmaps are
-    // cleared, and the set-up barriers order LDS only, so the query, ledger
-    // and first key loads are all in flight together.  The counts are of the
-    // ledger's filled slots.
+    // cleared, and the set-up barriers order LDS only, so the query and
+    // ledger loads are in flight together.  The counts are of the ledger's
+    // filled slots.
     constexpr int RPW = BM / C::NWV;
     auto load_chunk = [&](int s0, int (&id)[RPW]) {
         const int slot = s0 + lane;
