@@ -103,15 +103,19 @@ __global__ __launch_bounds__(kDenseThreads) void rescore_dense_kernel(RescoreArg
     // filled slots.
     constexpr int RPW = BM / C::NWV;
     auto load_chunk = [&](int s0, int (&id)[RPW]) {
+        // the lane's column of the ledger (routes or sentinels) and its row
+        // stride, formed once, so the unrolled loads need no kernel argument
         const int slot = s0 + lane;
         const bool inr = slot < a.k, live = slot < c_led;
+        const int32_t *col = inr ? a.led_routes + slot : (live ? a.led_sent + (slot - a.k) : a.led_routes);
+        const int64_t stride = inr ? a.k : (live ? c_sent : a.k);
+        const int nrow = min(BM, a.n_q - i0);  // rows of the tile
 #pragma unroll
         for (int q = 0; q < RPW; ++q) {
             const int r = w + q * C::NWV;
-            const int64_t row = (i0 + r < a.n_q) ? g0 + r : g0;
-            const int32_t *src = inr ? a.led_routes + row * a.k + slot
-                                     : (live ? a.led_sent + row * c_sent + (slot - a.k) : a.led_routes + g0 * a.k);
-            id[q] = (i0 + r < a.n_q && live) ? *src : -1;
+            const bool ok = live && r < nrow;
+            const int v = col[(g0 + (ok ? r : 0)) * stride];
+            id[q] = ok ? v : -1;
         }
     };
     int id[RPW];
