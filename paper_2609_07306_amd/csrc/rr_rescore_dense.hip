@@ -85,8 +85,18 @@ __global__ __launch_bounds__(kDenseThreads) void rescore_dense_kernel(RescoreArg
     const int64_t g0 = (int64_t)h * a.n_q + i0;  // first row of the tile
     const int c_sent = a.m + a.r, c_led = a.k + c_sent;
 
-    // the query fragments are requested first: their latency overlaps the
-    // bitmap set-up
+    // the tile's longest valid key range (tiles always hold a row), and the
+    // first two key stages, the query fragments and the ledger rows are all
+    // requested before the bitmap set-up, whose barriers order LDS only
+    const int ncols = a.causal ? min(min(i0 + BM, a.n_q), a.n_k) : a.n_k;
+    const int nb = __builtin_amdgcn_readfirstlane((ncols + 32 * KS - 1) / (32 * KS));
+    const int seg = 16 * nb;
+    const unsigned char *Kg = reinterpret_cast<const unsigned char *>(a.K) +
+                              (int64_t)(h / (a.n_heads / a.n_kv_heads)) * a.n_k * C::ROWB;
+    // double-buffered key fragments where a second set fits in registers
+    constexpr bool kDb = sizeof(DT) * D <= 256;
+    u32x4_t breg[2][C::PER_T];
+    if constexpr (kDb) route_detail::sweep_db_first<C>(breg, Kg, a.n_k, seg, nb, tid);
     const int myrow = 32 * rb + l32;
     Frag<DT, D> fq;
     if (i0 + myrow < a.n_q)
@@ -154,22 +164,15 @@ __global__ __launch_bounds__(kDenseThreads) void rescore_dense_kernel(RescoreArg
         }
     }
     lds_barrier();
-    // the tile's longest valid key range (tiles always hold a row)
-    const int ncols = a.causal ? min(min(i0 + BM, a.n_q), a.n_k) : a.n_k;
-    const int nb = __builtin_amdgcn_readfirstlane((ncols + 32 * KS - 1) / (32 * KS));
-    const int seg = 16 * nb;
 
     const int myseg = 2 * p + hh;
-    const unsigned char *Kg = reinterpret_cast<const unsigned char *>(a.K) +
-                              (int64_t)(h / (a.n_heads / a.n_kv_heads)) * a.n_k * C::ROWB;
     DenseEpi epi;
     epi.amin = INFINITY;
     epi.bmax = -INFINITY;
     epi.sbase = myseg * seg;
     epi.bmr = bm + myrow * nwd;
-    // double-buffered key fragments where a second set fits in registers
-    if constexpr (sizeof(DT) * D <= 256)
-        route_detail::sweep_keys_db<DT, D, C>(fq, Kg, a.n_k, seg, nb, nb, tid, p, hh, l32, bt, epi);
+    if constexpr (kDb)
+        route_detail::sweep_keys_db<DT, D, C>(fq, Kg, a.n_k, seg, nb, nb, tid, p, hh, l32, bt, breg, epi);
     else
         route_detail::sweep_keys<DT, D, C>(fq, Kg, a.n_k, seg, nb, nb, tid, p, hh, l32, bt, epi);
 
