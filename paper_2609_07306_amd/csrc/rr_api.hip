@@ -10,6 +10,7 @@
 
 #include "routerelay.h"
 #include "rr_internal.hpp"
+#include "rr_rescore.hpp"
 
 struct rr_ledger {
     rr_config cfg;

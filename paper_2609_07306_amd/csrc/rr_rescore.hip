@@ -26,6 +26,7 @@
 
 #include "rr_device.hpp"
 #include "rr_internal.hpp"
+#include "rr_rescore.hpp"
 
 namespace rr {
 namespace {
@@ -259,7 +260,8 @@ hipError_t launch_d(const RescoreArgs &a, hipStream_t stream)
 void rescore_geometry(int64_t rows, int n_q, int n_k, RescoreGeometry &g)
 {
     // dense tiles when the key range is short enough for the bitmaps and the
-    // tiles fill the chip; otherwise the gather kernel
+    // tiles fill at least half the chip (measured: dense wins at 128 tiles of
+    // n_k = 512, the gather at 64 tiles of n_k = 256); otherwise the gather
     const int64_t tiles = (rows / n_q) * ((n_q + rescore_dense_tile_rows() - 1) / rescore_dense_tile_rows());
     g.dense = n_k <= kRescoreDenseMaxKeys && tiles >= kRescoreDenseMinTiles;
     if (g.dense) {

@@ -22,6 +22,7 @@
 // score-pair counts (score pairs follow the method's accounting: the ledger's
 // candidates, plus n_i for each refreshed row).
 
+#include "rr_rescore.hpp"
 #include "rr_route_impl.hpp"
 
 namespace rr {
