@@ -21,6 +21,7 @@ struct rr_ledger {
     int32_t *routes, *sent, *build, *age, *ids, *stat_nrr;
     uint8_t *flags;
     float *alpha, *beta;
+    float *seed_bound, *seed_rmax;  // dense rescoring -> reroute: per-row threshold seeds (or null)
     int64_t *blk_pairs;  // rescoring workgroup partials, consumed by the reroute kernel
     int32_t *blk_count;
     int64_t *stat_pairs;
@@ -107,7 +108,8 @@ rr_status alloc(T **p, int64_t n, const char *what)
 void free_all(rr_ledger *L)
 {
     void *ptrs[] = {L->routes, L->sent,  L->build,     L->age,       L->ids,       L->stat_nrr,
-                    L->flags,  L->alpha, L->beta,      L->blk_pairs, L->blk_count, L->stat_pairs};
+                    L->flags,  L->alpha, L->beta,      L->blk_pairs, L->blk_count, L->stat_pairs,
+                    L->seed_bound, L->seed_rmax};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);
 }
@@ -233,6 +235,17 @@ rr_status rr_ledger_create(const rr_config *cfg, rr_ledger **out)
         delete L;
         return st;
     }
+    // threshold seeds: only where the relay layers rescore with dense tiles
+    // that compute them
+    rr::RescoreGeometry geo;
+    rr::rescore_geometry(rows, cfg->n_q, cfg->n_k, geo);
+    if (geo.dense && rr::rescore_dense_seeds(cfg->dtype, cfg->d) &&
+        ((st = alloc(&L->seed_bound, rows, "seed bounds")) != RR_OK ||
+         (st = alloc(&L->seed_rmax, rows, "seed maxima")) != RR_OK)) {
+        free_all(L);
+        delete L;
+        return st;
+    }
     // One-time initialisation (outside any hot path): an empty ledger.
     hipError_t e = hipSuccess;
     if (e == hipSuccess) e = hipMemset(L->routes, 0xFF, sizeof(int32_t) * rows * cfg->k);
@@ -328,6 +341,8 @@ rr_status rr_relay_layer(rr_ledger *L, int32_t layer, const void *Qc, const void
     s.beta = L->beta;
     s.blk_pairs = L->blk_pairs;
     s.blk_count = L->blk_count;
+    s.seed_bound = L->seed_bound;
+    s.seed_rmax = L->seed_rmax;
     hipError_t e = timed(RR_KERNEL_RESCORE, stream, [&] { return rr::launch_rescore(s, c.dtype, stream); });
     if (e != hipSuccess) return hip_fail(e, "rescore launch");
 
@@ -347,6 +362,8 @@ rr_status rr_relay_layer(rr_ledger *L, int32_t layer, const void *Qc, const void
     a.pairs_out = pairs;
     a.nrr_out = n_rerouted;
     a.ids_out = L->ids;
+    a.seed_bound = L->seed_bound;
+    a.seed_rmax = L->seed_rmax;
     const int rt = rr::route_tile_rows(c.k + c.m);
     const int max_tiles = c.n_heads * ((c.n_q + rt - 1) / rt);
     const int grid8 = (max_tiles + 7) & ~7;  // a multiple of 8: per-XCD tile ranges

@@ -42,6 +42,8 @@ struct RouteArgs {
     int32_t *stat_nrr;         // reroute: the call's rerouted rows (ledger copy)
     int32_t *nrr_out;          // reroute: optional device scalar
     int32_t *ids_out;          // reroute: compacted row ids per head, or null
+    const float *seed_bound;   // reroute, or null: per row, a lower bound of its T-th score ...
+    const float *seed_rmax;    // ... and its largest score, from the rescoring pass (no threshold sweep)
     int64_t *pairs_out;        // optional device scalar
     int64_t pairs_value;       // value written to pairs_out (full / anchor; reroute: the workgroup sums)
 };

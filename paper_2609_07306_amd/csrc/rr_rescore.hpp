@@ -36,6 +36,8 @@ struct RescoreArgs {
     float *beta;
     int64_t *blk_pairs;  // [n_heads * blocks_per_head] score pairs per workgroup (head-major)
     int32_t *blk_count;  // [n_heads * blocks_per_head] flagged rows per workgroup
+    float *seed_bound;   // dense, or null: [rows] a lower bound of the row's (k+m)-th score
+    float *seed_rmax;    // dense, or null: [rows] the row's largest score
 };
 
 // Launch shape of the rescoring kernel for a configuration.
@@ -47,6 +49,7 @@ struct RescoreGeometry {
 void rescore_geometry(int64_t rows, int n_q, int n_k, RescoreGeometry &g);
 hipError_t launch_rescore(const RescoreArgs &a, int dtype, hipStream_t stream);
 int rescore_dense_tile_rows();
+bool rescore_dense_seeds(int dtype, int d);  // the dense kernel writes seed_bound / seed_rmax
 hipError_t launch_rescore_dense(const RescoreArgs &a, int dtype, hipStream_t stream);
 
 }  // namespace rr

@@ -22,6 +22,8 @@
 // score-pair counts (score pairs follow the method's accounting: the ledger's
 // candidates, plus n_i for each refreshed row).
 
+#include <algorithm>
+
 #include "rr_rescore.hpp"
 #include "rr_route_impl.hpp"
 
@@ -35,14 +37,25 @@ constexpr int kDenseRowBlocks = 4;
 constexpr int kDenseThreads = 64 * kDenseRowBlocks * 2;
 template <typename DT, int D>
 using DenseRT = RT<DT, D, kDenseRowBlocks, 2, 2, 64, 32>;
+// Tiles whose key fragments take at most 256 bytes per row have the
+// registers for the kept scores of the threshold step as well.
+template <typename DT, int D>
+constexpr bool kDenseSeeds = sizeof(DT) * D <= 256;
 
+// SEED: the epilogue also keeps, per register slot, the top two scores of
+// the valid keys passing through it (the routing kernel's threshold sweep),
+// from which each row's bound of its (k+m)-th score and its maximum follow.
+template <bool SEED>
 struct DenseEpi {
     float amin, bmax;
     int sbase;         // first key of the lane's segment
     const uint2 *bmr;  // this lane's row: (R word, C word) per 32 keys
+    int nrow;          // SEED: valid keys of the lane's row (0: padding row)
+    float top[SEED ? 16 : 1][2];
 
     template <class F>
-    __device__ __forceinline__ void step(int st, const f32x16_t &acc, f32x16_t &next, const F &fq, const F &fk, bool)
+    __device__ __forceinline__ void step(int st, const f32x16_t &acc, f32x16_t &next, const F &fq, const F &fk,
+                                         bool full)
     {
         const int k0 = sbase + 16 * st;  // this lane's keys: k0 .. k0 + 15 (k0 % 16 == 0)
         const uint2 wv = bmr[k0 >> 5];
@@ -58,7 +71,17 @@ struct DenseEpi {
             amin = fminf(amin, __uint_as_float((xb & nr) | (0x7F800000u & ~nr)));  // +inf when out
             bmax = fmaxf(bmax, __uint_as_float((xb & nc) | (0xFF800000u & ~nc)));  // -inf when out
         }
-        route_detail::interleave_mfma<F::NS, (16 * 6 + F::NS - 1) / F::NS>();
+        if constexpr (SEED) {
+            if (full) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i) route_detail::top_insert<2>(top[i], acc[i]);
+            } else {
+                const int vlim = nrow - k0;  // keys k0 + i are valid for i < vlim
+#pragma unroll
+                for (int i = 0; i < 16; ++i) route_detail::top_insert<2>(top[i], (i < vlim) ? acc[i] : -INFINITY);
+            }
+        }
+        route_detail::interleave_mfma<F::NS, (16 * (SEED ? 8 : 6) + F::NS - 1) / F::NS>();
     }
 };
 
@@ -67,13 +90,14 @@ __global__ __launch_bounds__(kDenseThreads) void rescore_dense_kernel(RescoreArg
 {
     using C = DenseRT<DT, D>;
     static_assert(C::NT == kDenseThreads, "launch bounds of the tile shape");
+    constexpr bool SEED = kDenseSeeds<DT, D>;
     constexpr int BM = C::BM, NT = C::NT, NW = kDenseRowBlocks, KS = 2;
     constexpr int NWB = (BM + 63) / 64;  // waves holding one lane per row
     extern __shared__ __align__(16) unsigned char smem[];
     unsigned char *bt = smem;                                     // [2][KS][32][BSTR] key tiles
     uint2 *bm = reinterpret_cast<uint2 *>(smem + 2 * C::ST);      // [BM][bm_words] (R word, C word) pairs
     __shared__ int32_t row_n[BM], s_nc[BM], s_ns[BM];
-    __shared__ float s_amin[KS][BM], s_bmax[KS][BM];
+    __shared__ float s_amin[KS][BM], s_bmax[KS][BM], s_b1[BM], s_rmx[BM];
     __shared__ unsigned long long s_pairs[NWB];
     __shared__ unsigned s_cnt[NWB];
 
@@ -99,6 +123,20 @@ __global__ __launch_bounds__(kDenseThreads) void rescore_dense_kernel(RescoreArg
     u32x4_t breg[2][C::PER_T];
     if constexpr (kDb) route_detail::sweep_db_first<C>(breg, Kg, a.n_k, seg, nb, tid);
     const int myrow = 32 * rb + l32;
+    const int myseg = 2 * p + hh;
+    const int mi = i0 + myrow;
+    const int nrow = (mi < a.n_q) ? (a.causal ? min(mi + 1, a.n_k) : a.n_k) : 0;
+    // stages whose keys (up to (2p+1)*seg + 16 st + 15) are valid for every
+    // row of the wave (the kept scores mask the others)
+    int full_stages = nb;
+    if constexpr (SEED) {
+        int minn = (mi < a.n_q) ? nrow : INT_MAX;
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) minn = min(minn, __shfl_xor(minn, off, 64));
+        const int slack = minn - (2 * p + 1) * seg - 16;
+        full_stages = __builtin_amdgcn_readfirstlane(
+            (minn == INT_MAX) ? nb : (slack < 0 ? 0 : min(nb, slack / 16 + 1)));
+    }
     Frag<DT, D> fq;
     if (i0 + myrow < a.n_q)
         fq.load(reinterpret_cast<const DT *>(a.Q) + (g0 + myrow) * D, hh);
@@ -166,16 +204,20 @@ __global__ __launch_bounds__(kDenseThreads) void rescore_dense_kernel(RescoreArg
     }
     lds_barrier();
 
-    const int myseg = 2 * p + hh;
-    DenseEpi epi;
+    DenseEpi<SEED> epi;
     epi.amin = INFINITY;
     epi.bmax = -INFINITY;
     epi.sbase = myseg * seg;
     epi.bmr = bm + myrow * nwd;
+    epi.nrow = nrow;
+    if constexpr (SEED) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) epi.top[i][0] = epi.top[i][1] = -INFINITY;
+    }
     if constexpr (kDb)
-        route_detail::sweep_keys_db<DT, D, C>(fq, Kg, a.n_k, seg, nb, nb, tid, p, hh, l32, bt, breg, epi);
+        route_detail::sweep_keys_db<DT, D, C>(fq, Kg, a.n_k, seg, nb, full_stages, tid, p, hh, l32, bt, breg, epi);
     else
-        route_detail::sweep_keys<DT, D, C>(fq, Kg, a.n_k, seg, nb, nb, tid, p, hh, l32, bt, epi);
+        route_detail::sweep_keys<DT, D, C>(fq, Kg, a.n_k, seg, nb, full_stages, tid, p, hh, l32, bt, epi);
 
     // the row's four lanes: halves hh of a wave, then the key splits p
     float amin = fminf(epi.amin, __shfl_xor(epi.amin, 32, 64));
@@ -184,7 +226,16 @@ __global__ __launch_bounds__(kDenseThreads) void rescore_dense_kernel(RescoreArg
         s_amin[p][myrow] = amin;
         s_bmax[p][myrow] = bmax;
     }
-    __syncthreads();
+    __syncthreads();  // (also: every wave is done with the key tiles and bitmaps)
+    if constexpr (SEED) {
+        // the routing kernel's threshold step on the same scores: kept sets
+        // -> bound of the (k+m)-th score and the row maximum
+        float *us = reinterpret_cast<float *>(smem);
+        route_detail::store_kept<C, 2>(us, myrow, myseg, epi.top);
+        __syncthreads();
+        route_detail::bound_of_kept<C>(us, tid, a.k + a.m, s_b1, s_rmx);
+        __syncthreads();
+    }
 
     unsigned long long pairs_t = 0;
     unsigned cnt_t = 0;
@@ -199,6 +250,10 @@ __global__ __launch_bounds__(kDenseThreads) void rescore_dense_kernel(RescoreArg
         a.alpha[row] = al;
         a.beta[row] = be;
         if (!flag) a.led_age[row] = a.layer - a.led_build[row];
+        if (SEED && a.seed_bound) {
+            a.seed_bound[row] = s_b1[tid];
+            a.seed_rmax[row] = s_rmx[tid];
+        }
         pairs_t = (unsigned long long)(nc + ns + (flag ? row_n[tid] : 0));
         cnt_t = flag ? 1u : 0u;
     }
@@ -232,7 +287,8 @@ template <typename DT, int D>
 hipError_t launch_d(const RescoreArgs &a, hipStream_t stream)
 {
     using C = DenseRT<DT, D>;
-    const size_t lds = (size_t)2 * C::ST + (size_t)C::BM * a.bm_words * sizeof(uint2);
+    size_t lds = (size_t)2 * C::ST + (size_t)C::BM * a.bm_words * sizeof(uint2);
+    if (kDenseSeeds<DT, D>) lds = std::max(lds, (size_t)C::BM * C::UST * sizeof(float));  // the kept scores
     const void *fn = reinterpret_cast<const void *>(&rescore_dense_kernel<DT, D>);
     if (lds > 65536) {
         const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -246,6 +302,11 @@ hipError_t launch_d(const RescoreArgs &a, hipStream_t stream)
 }  // namespace
 
 int rescore_dense_tile_rows() { return DenseRT<float, 32>::BM; }
+
+bool rescore_dense_seeds(int dtype, int d)
+{
+    return (dtype == 0 ? kDenseSeeds<float, 64> : kDenseSeeds<bf16_t, 128>) && (dtype == 0 ? 4 : 2) * d <= 256;
+}
 
 hipError_t launch_rescore_dense(const RescoreArgs &a, int dtype, hipStream_t stream)
 {

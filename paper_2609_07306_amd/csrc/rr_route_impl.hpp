@@ -71,6 +71,7 @@ namespace route_detail {
 
 constexpr int kMaxFixIters = 64;  // bound on collection sweeps per tile (score + id bisection need <= 50)
 constexpr int kBisect = 10;       // bisection steps of the threshold bound
+constexpr uint32_t kSeedSlack = 8;  // orders by which a reroute widens the rescoring pass's bound and maximum
 constexpr int kPrefetch = 2;      // key stages in flight ahead of the MFMA
 constexpr int kBmWords = 64;      // bitmap words per row (exact for n_i <= 2048)
 constexpr int kBmStride = 65;     // odd row stride: rows fall in different banks
@@ -439,6 +440,79 @@ struct TopEpi {
     }
 };
 
+// The lane's 16 x TT kept scores -> its segment's part of the row's kept
+// set in LDS (rows of UST floats).
+template <class C, int TT>
+__device__ __forceinline__ void store_kept(float *us, int myrow, int myseg, const float (&top)[16][TT])
+{
+    float *U = us + myrow * C::UST + myseg * 16 * TT;
+#pragma unroll
+    for (int q = 0; q < 4 * TT; ++q) {
+        float4 x;
+        x.x = top[(4 * q + 0) / TT][(4 * q + 0) % TT];
+        x.y = top[(4 * q + 1) / TT][(4 * q + 1) % TT];
+        x.z = top[(4 * q + 2) / TT][(4 * q + 2) % TT];
+        x.w = top[(4 * q + 3) / TT][(4 * q + 3) % TT];
+        reinterpret_cast<float4 *>(U)[q] = x;
+    }
+}
+
+// Bound of the row's T-th score from its kept set U, LPR neighbouring
+// threads per row (UPL kept scores each): any v with |{u in U : u >= v}| >= T
+// is at most the row's T-th score; start from the smallest finite entry of U
+// when U holds at least T of them (else -inf, which admits every valid chunk)
+// and bisect toward the row maximum, which is U's largest entry.  Thread
+// part 0 of row r stores the bound and the maximum into b1[r] and rmax[r].
+template <class C>
+__device__ __forceinline__ void bound_of_kept(const float *us, int tid, int T, float *b1, float *rmx)
+{
+    const int r = tid / C::LPR, part = tid % C::LPR;
+    float u[C::UPL];
+    const float4 *ur = reinterpret_cast<const float4 *>(us + r * C::UST + part * C::UPL);
+#pragma unroll
+    for (int q = 0; q < C::UPL / 4; ++q) {
+        const float4 x = ur[q];
+        u[4 * q] = x.x;
+        u[4 * q + 1] = x.y;
+        u[4 * q + 2] = x.z;
+        u[4 * q + 3] = x.w;
+    }
+    float rmax = -INFINITY, umin = INFINITY;
+    int nfin = 0;
+#pragma unroll
+    for (int q = 0; q < C::UPL; ++q) {
+        const bool fin = u[q] > -INFINITY;
+        rmax = fmaxf(rmax, u[q]);
+        umin = fminf(umin, fin ? u[q] : INFINITY);
+        nfin += fin ? 1 : 0;
+    }
+#pragma unroll
+    for (int off = 1; off < C::LPR; off <<= 1) {
+        rmax = fmaxf(rmax, __shfl_xor(rmax, off, 64));
+        umin = fminf(umin, __shfl_xor(umin, off, 64));
+        nfin += __shfl_xor(nfin, off, 64);
+    }
+    float lo = (nfin >= T) ? umin : -INFINITY, hi = rmax;
+    if (lo > -INFINITY) {
+        for (int it = 0; it < kBisect; ++it) {
+            const float mid = lo + 0.5f * (hi - lo);
+            int cnt = 0;
+#pragma unroll
+            for (int q = 0; q < C::UPL; ++q) cnt += (u[q] >= mid) ? 1 : 0;
+#pragma unroll
+            for (int off = 1; off < C::LPR; off <<= 1) cnt += __shfl_xor(cnt, off, 64);
+            if (cnt >= T)
+                lo = mid;
+            else
+                hi = mid;
+        }
+    }
+    if (part == 0) {
+        b1[r] = lo;
+        rmx[r] = rmax;
+    }
+}
+
 // Collection-sweep epilogue: the lane appends the scores of its segment that
 // reach its row's threshold to its sub-list.  A chunk is admitted when
 // s > th, or s == th and its id is at most th_id; th_id is INT_MAX except
@@ -678,81 +752,39 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
             fq.zero();
 
         // ------------------------------------------------ sweep 1: thresholds
-        {
-            TopEpi<TT> epi;
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-#pragma unroll
-                for (int j = 0; j < TT; ++j) epi.top[i][j] = -INFINITY;
-            }
-            epi.nrow = nrow;
-            epi.sbase = sbase;
-            sweep_keys<DT, D, C>(fq, Kg, a.n_k, seg, nb, full_stages, tid, p, hh, l32, bt, epi);
-            __syncthreads();  // every wave is done with the key tiles
-            // the lane's 16 x TT kept scores -> its segment's part of the row
-            float *U = us + myrow * C::UST + myseg * 16 * TT;
-#pragma unroll
-            for (int q = 0; q < 4 * TT; ++q) {
-                float4 x;
-                x.x = epi.top[(4 * q + 0) / TT][(4 * q + 0) % TT];
-                x.y = epi.top[(4 * q + 1) / TT][(4 * q + 1) % TT];
-                x.z = epi.top[(4 * q + 2) / TT][(4 * q + 2) % TT];
-                x.w = epi.top[(4 * q + 3) / TT][(4 * q + 3) % TT];
-                reinterpret_cast<float4 *>(U)[q] = x;
-            }
-        }
-        __syncthreads();
-        {
-            // LPR neighbouring lanes per row, UPL kept scores each
-            const int r = tid / C::LPR, part = tid % C::LPR;
-            float u[C::UPL];
-            const float4 *ur = reinterpret_cast<const float4 *>(us + r * C::UST + part * C::UPL);
-#pragma unroll
-            for (int q = 0; q < C::UPL / 4; ++q) {
-                const float4 x = ur[q];
-                u[4 * q] = x.x;
-                u[4 * q + 1] = x.y;
-                u[4 * q + 2] = x.z;
-                u[4 * q + 3] = x.w;
-            }
-            // Any v with |{x in U : x >= v}| >= T is at most the row's T-th
-            // score: start from the smallest finite entry of U when U holds
-            // at least T of them (else -inf, which admits every valid chunk)
-            // and bisect toward the row maximum, which is U's largest entry.
-            float rmax = -INFINITY, umin = INFINITY;
-            int nfin = 0;
-#pragma unroll
-            for (int q = 0; q < C::UPL; ++q) {
-                const bool fin = u[q] > -INFINITY;
-                rmax = fmaxf(rmax, u[q]);
-                umin = fminf(umin, fin ? u[q] : INFINITY);
-                nfin += fin ? 1 : 0;
-            }
-#pragma unroll
-            for (int off = 1; off < C::LPR; off <<= 1) {
-                rmax = fmaxf(rmax, __shfl_xor(rmax, off, 64));
-                umin = fminf(umin, __shfl_xor(umin, off, 64));
-                nfin += __shfl_xor(nfin, off, 64);
-            }
-            float lo = (nfin >= T) ? umin : -INFINITY, hi = rmax;
-            if (lo > -INFINITY) {
-                for (int it = 0; it < kBisect; ++it) {
-                    const float mid = lo + 0.5f * (hi - lo);
-                    int cnt = 0;
-#pragma unroll
-                    for (int q = 0; q < C::UPL; ++q) cnt += (u[q] >= mid) ? 1 : 0;
-#pragma unroll
-                    for (int off = 1; off < C::LPR; off <<= 1) cnt += __shfl_xor(cnt, off, 64);
-                    if (cnt >= T)
-                        lo = mid;
-                    else
-                        hi = mid;
+        if (mode == MODE_REROUTE && a.seed_bound) {
+            // the rescoring pass scored every key of these rows and left each
+            // row's bound and maximum; they are widened by kSeedSlack orders
+            // so that they hold even if its scores differ from this tile's in
+            // the last bits
+            if (tid < BM) {
+                const int64_t g = row_g[tid];
+                float b = -INFINITY, x = -INFINITY;
+                if (g >= 0) {
+                    b = a.seed_bound[g];
+                    x = a.seed_rmax[g];
+                    b = order_float(max(float_order(b) - kSeedSlack, float_order(-INFINITY)));
+                    x = order_float(min(float_order(x) + kSeedSlack, float_order(INFINITY)));
                 }
+                b1_s[tid] = b;
+                rmax_s[tid] = x;
             }
-            if (part == 0) {
-                b1_s[r] = lo;
-                rmax_s[r] = rmax;
+        } else {
+            {
+                TopEpi<TT> epi;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+#pragma unroll
+                    for (int j = 0; j < TT; ++j) epi.top[i][j] = -INFINITY;
+                }
+                epi.nrow = nrow;
+                epi.sbase = sbase;
+                sweep_keys<DT, D, C>(fq, Kg, a.n_k, seg, nb, full_stages, tid, p, hh, l32, bt, epi);
+                __syncthreads();  // every wave is done with the key tiles
+                store_kept<C, TT>(us, myrow, myseg, epi.top);
             }
+            __syncthreads();
+            bound_of_kept<C>(us, tid, T, b1_s, rmax_s);
         }
         __syncthreads();
         if (tid < BM) {
