@@ -21,6 +21,7 @@ subset of the same workload on this host.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -68,6 +69,8 @@ def parse():
     ap.add_argument("--workload", default="scale", help="synth preset (scale, drift, gqa, longctx, tiny)")
     ap.add_argument("--n", type=int, default=None, help="chunk count override (n_q = n_k)")
     ap.add_argument("--rho", type=float, default=None)
+    ap.add_argument("--relay", default="auto", choices=("auto", "one_pass", "split"),
+                    help="relay schedule (auto: one pass for causal inputs, else rescoring + compacted reroute)")
     ap.add_argument("--cpu-heads", type=int, default=2, help="heads in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-full", action="store_true", help="skip the full-routing baseline")
@@ -125,7 +128,7 @@ def main():
     if args.rho is not None:
         kw["rho"] = args.rho
     w = synth.preset(args.workload, **kw)
-    cfg = rr.Config.of(w)
+    cfg = dataclasses.replace(rr.Config.of(w), relay=args.relay)
     rows, L = cfg.rows, w.n_layers
     e_bytes = 2 if w.dtype == "bf16" else 4
     print(f"[bench] generating {describe(w)}", file=sys.stderr, flush=True)
@@ -240,6 +243,8 @@ def main():
         "anchor": ("mfma", 2.0 * w.d * full_pairs_layer / 1e12, "TFLOP/s", mpeak),
         "reroute": ("mfma", 2.0 * w.d * mean_rerouted * mean_ni / 1e12, "TFLOP/s", mpeak),
         "full": ("mfma", 2.0 * w.d * full_pairs_layer / 1e12, "TFLOP/s", mpeak),
+        # one-pass relay: the ledger's candidates rescored, the flagged rows routed
+        "relay": ("mfma", 2.0 * w.d * (rows * c + mean_rerouted * mean_ni) / 1e12, "TFLOP/s", mpeak),
     }
     kernels = {}
     for kind, (tms, n) in prof.items():
@@ -252,14 +257,15 @@ def main():
                          "bound": bound, "achieved": round(achieved, 3), "unit": unit,
                          "peak": peak, "frac": round(achieved / peak, 4),
                          "share_of_step": None}
-    path_ms = sum(prof[k][0] for k in ("anchor", "reroute", "rescore")) / args.steps
-    for kind in ("anchor", "reroute", "rescore"):
+    path_kinds = ("anchor", "reroute", "rescore", "relay")
+    path_ms = sum(prof[k][0] for k in path_kinds) / args.steps
+    for kind in path_kinds:
         if kind in kernels:
             kernels[kind]["share_of_step"] = round(prof[kind][0] / args.steps / ms_step, 4)
-    dom = max(("anchor", "reroute", "rescore"), key=lambda k: prof[k][0])
+    dom = max(path_kinds, key=lambda k: prof[k][0])
     dk = kernels[dom]
     # the recorded counters belong to the default workload (routing scale, n = 1024)
-    default_workload = args.workload == "scale" and w.n == 1024 and args.rho is None
+    default_workload = args.workload == "scale" and w.n == 1024 and args.rho is None and args.relay == "auto"
     roofline = {"kernel": dom, "bound": dk["bound"], "achieved": dk["achieved"], "peak": dk["peak"],
                 "unit": dk["unit"], "frac": dk["frac"],
                 "traffic": recorded_traffic(dom) if default_workload else None}

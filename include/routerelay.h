@@ -61,6 +61,21 @@ typedef enum { RR_F32 = 0, RR_BF16 = 1 } rr_dtype;
  * margin of Eq. (8); the paper uses gamma >= 0 (0 by default, Table 1);
  * +INFINITY refreshes every row that has a sentinel and -INFINITY refreshes
  * none.  seed keys the random-sentinel probes. */
+/* Options (rr_config.options).  A relay layer (Sec. 3.2) runs as one of two
+ * schedules with the same results:
+ *   one pass -- over the 128-row (or 64-row) tiles of every head, the tile's
+ *     scores rescore its rows' ledgers, the trigger flags rows, and the same
+ *     pass routes the flagged ones (possible while a tile's ledger bitmaps
+ *     fit its LDS: n_k up to about 2048, d = 256 up to about 1900);
+ *   split -- rescoring and trigger, then the routing of the flagged rows
+ *     compacted per head (Sec. 4.2).
+ * By default causal inputs take the one pass where it fits (compaction would
+ * mix short and long rows in one tile) and the others the split schedule
+ * (measured faster there).  RR_OPT_SPLIT_RELAY forces the split schedule,
+ * RR_OPT_ONE_PASS_RELAY the one pass (RR_ERR_UNSUPPORTED where it does not
+ * fit); not both. */
+typedef enum { RR_OPT_SPLIT_RELAY = 1, RR_OPT_ONE_PASS_RELAY = 2 } rr_option;
+
 typedef struct {
     int32_t n_heads;    /* H_q */
     int32_t n_kv_heads; /* H_kv */
@@ -73,7 +88,7 @@ typedef struct {
     int32_t dtype;      /* rr_dtype of Qc and Kc */
     int32_t causal;     /* 1: chunk mask j <= i */
     float gamma;        /* guard margin */
-    uint32_t reserved;  /* must be 0 */
+    uint32_t options;   /* rr_option bits (0: defaults) */
     uint64_t seed;
 } rr_config;
 
@@ -153,8 +168,8 @@ rr_status rr_ledger_import(rr_ledger *ledger, int32_t layer, const int32_t *rout
 
 /* Diagnostics of the most recent relay: per-row alpha and beta (binary32,
  * beta = -INFINITY for an empty C) and the compacted rerouted row ids, one
- * ascending list per head at ids[h*n_q .. h*n_q + count_h).  Each output
- * may be NULL. */
+ * ascending list per head at ids[h*n_q .. h*n_q + count_h), -1 after it
+ * (formed from the relay's flags when asked for).  Each output may be NULL. */
 rr_status rr_ledger_relay_stats(const rr_ledger *ledger, float *alpha, float *beta,
                                 int32_t *ids, void *hip_stream);
 
@@ -169,7 +184,8 @@ typedef enum {
     RR_KERNEL_ANCHOR = 1,   /* GEMM + TopK + ledger build, every row */
     RR_KERNEL_REROUTE = 2,  /* GEMM + TopK + ledger build, compacted rows */
     RR_KERNEL_RESCORE = 3,  /* rescoring (dense tiles or gather), trigger, compaction counts, ages */
-    RR_KERNEL_KINDS = 4
+    RR_KERNEL_RELAY = 4,    /* one-pass relay: rescoring + trigger + GEMM + TopK + ledger build of the flagged rows */
+    RR_KERNEL_KINDS = 5
 } rr_kernel_kind;
 
 rr_status rr_profile_start(void);

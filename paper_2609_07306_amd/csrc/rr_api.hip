@@ -18,10 +18,13 @@ struct rr_ledger {
     bool has_state;
     int32_t last_layer;
     int64_t rows;
-    int32_t *routes, *sent, *build, *age, *ids, *stat_nrr;
+    int32_t *routes, *sent, *build, *age, *stat_nrr;
     uint8_t *flags;
     float *alpha, *beta;
     float *seed_bound, *seed_rmax;  // dense rescoring -> reroute: per-row threshold seeds (or null)
+    bool fused;                     // relay layers as one pass (else rescoring + compacted reroute)
+    int32_t bm_words;               // fused: ledger bitmap row stride in (R, C) word pairs
+    uint32_t *done;                 // fused: finished-workgroup counter of the relay pass
     int64_t *blk_pairs;  // rescoring workgroup partials, consumed by the reroute kernel
     int32_t *blk_count;
     int64_t *stat_pairs;
@@ -30,6 +33,35 @@ struct rr_ledger {
 namespace {
 
 thread_local std::string g_err;
+
+// Diagnostics: the flagged rows of each head as an ascending id list
+// (ballot + prefix over the head's flags), -1 after the last.  One
+// workgroup per head.
+constexpr int kIdsThreads = 256;
+__global__ __launch_bounds__(kIdsThreads) void flagged_ids_kernel(const uint8_t *flags, int n_q, int32_t *ids)
+{
+    __shared__ int s_wave[kIdsThreads / 64];
+    const uint8_t *f = flags + (int64_t)blockIdx.x * n_q;
+    int32_t *o = ids + (int64_t)blockIdx.x * n_q;
+    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    int base = 0;
+    for (int i0 = 0; i0 < n_q; i0 += kIdsThreads) {
+        const int i = i0 + (int)threadIdx.x;
+        const bool fl = i < n_q && f[i] != 0;
+        const uint64_t mk = __ballot(fl);
+        if (lane == 0) s_wave[w] = __popcll(mk);
+        __syncthreads();
+        int pre = base, tot = 0;
+        for (int v = 0; v < kIdsThreads / 64; ++v) {
+            pre += (v < w) ? s_wave[v] : 0;
+            tot += s_wave[v];
+        }
+        if (fl) o[pre + __popcll(mk & ((1ull << lane) - 1ull))] = i;
+        base += tot;
+        __syncthreads();
+    }
+    for (int j = base + (int)threadIdx.x; j < n_q; j += kIdsThreads) o[j] = -1;
+}
 
 rr_status fail(rr_status s, const std::string &msg)
 {
@@ -56,7 +88,10 @@ int64_t full_pairs(const rr_config &c)
 rr_status validate(const rr_config *c, bool ledger)
 {
     if (!c) return fail(RR_ERR_INVALID, "config is NULL");
-    if (c->reserved != 0) return fail(RR_ERR_INVALID, "config.reserved must be 0");
+    if ((c->options & ~(uint32_t)(RR_OPT_SPLIT_RELAY | RR_OPT_ONE_PASS_RELAY)) != 0)
+        return fail(RR_ERR_INVALID, "unknown config.options bits");
+    if ((c->options & RR_OPT_SPLIT_RELAY) && (c->options & RR_OPT_ONE_PASS_RELAY))
+        return fail(RR_ERR_INVALID, "RR_OPT_SPLIT_RELAY and RR_OPT_ONE_PASS_RELAY exclude each other");
     if (c->n_heads < 1 || c->n_kv_heads < 1 || c->n_heads % c->n_kv_heads != 0)
         return fail(RR_ERR_INVALID, "n_heads must be a positive multiple of n_kv_heads");
     if (c->n_q < 1 || c->n_k < 1) return fail(RR_ERR_INVALID, "n_q and n_k must be >= 1");
@@ -107,7 +142,7 @@ rr_status alloc(T **p, int64_t n, const char *what)
 
 void free_all(rr_ledger *L)
 {
-    void *ptrs[] = {L->routes, L->sent,  L->build,     L->age,       L->ids,       L->stat_nrr,
+    void *ptrs[] = {L->routes, L->sent,  L->build,     L->age,       L->done,      L->stat_nrr,
                     L->flags,  L->alpha, L->beta,      L->blk_pairs, L->blk_count, L->stat_pairs,
                     L->seed_bound, L->seed_rmax};
     for (void *p : ptrs)
@@ -225,7 +260,7 @@ rr_status rr_ledger_create(const rr_config *cfg, rr_ledger **out)
     if ((st = alloc(&L->routes, rows * cfg->k, "routes")) != RR_OK ||
         (st = alloc(&L->sent, rows * (cfg->m + cfg->r), "sentinels")) != RR_OK ||
         (st = alloc(&L->build, rows, "build")) != RR_OK || (st = alloc(&L->age, rows, "age")) != RR_OK ||
-        (st = alloc(&L->ids, rows, "ids")) != RR_OK || (st = alloc(&L->stat_nrr, 1, "stat_nrr")) != RR_OK ||
+        (st = alloc(&L->stat_nrr, 1, "stat_nrr")) != RR_OK ||
         (st = alloc(&L->flags, rows, "flags")) != RR_OK || (st = alloc(&L->alpha, rows, "alpha")) != RR_OK ||
         (st = alloc(&L->beta, rows, "beta")) != RR_OK ||
         (st = alloc(&L->blk_pairs, max_blocks, "rescore partials")) != RR_OK ||
@@ -235,13 +270,25 @@ rr_status rr_ledger_create(const rr_config *cfg, rr_ledger **out)
         delete L;
         return st;
     }
-    // threshold seeds: only where the relay layers rescore with dense tiles
-    // that compute them
+    // relay layers in one pass where a tile's ledger bitmaps (R and C words
+    // over the padded key range, odd row stride) fit its LDS, by default for
+    // causal inputs only; otherwise threshold seeds where the rescoring
+    // kernel's dense tiles compute them
+    L->bm_words = 2 * ((cfg->n_k + 63) / 64) + 1;
+    const bool fits = L->bm_words <= rr::route_relay_max_bm_words(cfg->dtype, cfg->d, cfg->k + cfg->m);
+    if ((cfg->options & RR_OPT_ONE_PASS_RELAY) && !fits) {
+        free_all(L);
+        delete L;
+        return fail(RR_ERR_UNSUPPORTED, "one-pass relay: the ledger bitmaps of a tile exceed its LDS (n_k too large)");
+    }
+    L->fused = fits && ((cfg->options & RR_OPT_ONE_PASS_RELAY) ||
+                        (!(cfg->options & RR_OPT_SPLIT_RELAY) && cfg->causal));
     rr::RescoreGeometry geo;
     rr::rescore_geometry(rows, cfg->n_q, cfg->n_k, geo);
-    if (geo.dense && rr::rescore_dense_seeds(cfg->dtype, cfg->d) &&
-        ((st = alloc(&L->seed_bound, rows, "seed bounds")) != RR_OK ||
-         (st = alloc(&L->seed_rmax, rows, "seed maxima")) != RR_OK)) {
+    if ((L->fused && (st = alloc(&L->done, 1, "relay counter")) != RR_OK) ||
+        (!L->fused && geo.dense && rr::rescore_dense_seeds(cfg->dtype, cfg->d) &&
+         ((st = alloc(&L->seed_bound, rows, "seed bounds")) != RR_OK ||
+          (st = alloc(&L->seed_rmax, rows, "seed maxima")) != RR_OK))) {
         free_all(L);
         delete L;
         return st;
@@ -252,6 +299,7 @@ rr_status rr_ledger_create(const rr_config *cfg, rr_ledger **out)
     if (e == hipSuccess && cfg->m + cfg->r > 0) e = hipMemset(L->sent, 0xFF, sizeof(int32_t) * rows * (cfg->m + cfg->r));
     if (e == hipSuccess) e = hipMemset(L->build, 0xFF, sizeof(int32_t) * rows);
     if (e == hipSuccess) e = hipMemset(L->age, 0, sizeof(int32_t) * rows);
+    if (e == hipSuccess && L->done) e = hipMemset(L->done, 0, sizeof(uint32_t));
     if (e == hipSuccess) e = hipDeviceSynchronize();
     if (e != hipSuccess) {
         free_all(L);
@@ -310,68 +358,95 @@ rr_status rr_relay_layer(rr_ledger *L, int32_t layer, const void *Qc, const void
     const rr_config &c = L->cfg;
     hipStream_t stream = reinterpret_cast<hipStream_t>(hip_stream);
 
-    rr::RescoreArgs s;
-    std::memset(&s, 0, sizeof(s));
-    s.Q = Qc;
-    s.K = Kc;
-    s.n_heads = c.n_heads;
-    s.n_kv_heads = c.n_kv_heads;
-    s.n_q = c.n_q;
-    s.n_k = c.n_k;
-    s.d = c.d;
-    s.k = c.k;
-    s.m = c.m;
-    s.r = c.r;
-    s.causal = c.causal;
-    s.layer = layer;
-    rr::RescoreGeometry geo;
-    rr::rescore_geometry(L->rows, c.n_q, c.n_k, geo);
-    s.blocks_per_head = geo.blocks_per_head;
-    s.rows_per_wave = geo.rows_per_wave;
-    s.dense = geo.dense ? 1 : 0;
-    s.bm_words = geo.bm_words;
-    s.gamma = c.gamma;
-    s.led_routes = L->routes;
-    s.led_sent = L->sent;
-    s.led_build = L->build;
-    s.led_age = L->age;
-    s.flags = L->flags;
-    s.mask_out = mask;
-    s.alpha = L->alpha;
-    s.beta = L->beta;
-    s.blk_pairs = L->blk_pairs;
-    s.blk_count = L->blk_count;
-    s.seed_bound = L->seed_bound;
-    s.seed_rmax = L->seed_rmax;
-    hipError_t e = timed(RR_KERNEL_RESCORE, stream, [&] { return rr::launch_rescore(s, c.dtype, stream); });
-    if (e != hipSuccess) return hip_fail(e, "rescore launch");
+    if (L->fused) {
+        // one pass: each tile rescores its rows' ledgers on its own scores,
+        // flags them, and routes the flagged rows into the ledger
+        rr::RouteArgs a = route_args(c, Qc, Kc);
+        a.layer = layer;
+        a.mode = rr::MODE_RELAY;
+        a.led_routes = L->routes;
+        a.led_sent = L->sent;
+        a.led_build = L->build;
+        a.led_age = L->age;
+        a.flags = L->flags;
+        a.mask_out = mask;
+        a.alpha_out = L->alpha;
+        a.beta_out = L->beta;
+        a.gamma = c.gamma;
+        a.bm_words = L->bm_words;
+        a.blk_pairs = L->blk_pairs;
+        a.blk_count = L->blk_count;
+        a.done = L->done;
+        a.stat_pairs = L->stat_pairs;
+        a.stat_nrr = L->stat_nrr;
+        a.pairs_out = pairs;
+        a.nrr_out = n_rerouted;
+        const int grid = c.n_heads * a.tiles_per_head;
+        hipError_t e = timed(RR_KERNEL_RELAY, stream, [&] { return rr::launch_route(a, c.dtype, grid, stream); });
+        if (e != hipSuccess) return hip_fail(e, "relay launch");
+    } else {
+        rr::RescoreArgs s;
+        std::memset(&s, 0, sizeof(s));
+        s.Q = Qc;
+        s.K = Kc;
+        s.n_heads = c.n_heads;
+        s.n_kv_heads = c.n_kv_heads;
+        s.n_q = c.n_q;
+        s.n_k = c.n_k;
+        s.d = c.d;
+        s.k = c.k;
+        s.m = c.m;
+        s.r = c.r;
+        s.causal = c.causal;
+        s.layer = layer;
+        rr::RescoreGeometry geo;
+        rr::rescore_geometry(L->rows, c.n_q, c.n_k, geo);
+        s.blocks_per_head = geo.blocks_per_head;
+        s.rows_per_wave = geo.rows_per_wave;
+        s.dense = geo.dense ? 1 : 0;
+        s.bm_words = geo.bm_words;
+        s.gamma = c.gamma;
+        s.led_routes = L->routes;
+        s.led_sent = L->sent;
+        s.led_build = L->build;
+        s.led_age = L->age;
+        s.flags = L->flags;
+        s.mask_out = mask;
+        s.alpha = L->alpha;
+        s.beta = L->beta;
+        s.blk_pairs = L->blk_pairs;
+        s.blk_count = L->blk_count;
+        s.seed_bound = L->seed_bound;
+        s.seed_rmax = L->seed_rmax;
+        hipError_t e = timed(RR_KERNEL_RESCORE, stream, [&] { return rr::launch_rescore(s, c.dtype, stream); });
+        if (e != hipSuccess) return hip_fail(e, "rescore launch");
 
-    rr::RouteArgs a = route_args(c, Qc, Kc);
-    a.layer = layer;
-    a.mode = rr::MODE_REROUTE;
-    a.led_routes = L->routes;
-    a.led_sent = L->sent;
-    a.led_build = L->build;
-    a.led_age = L->age;
-    a.flags = L->flags;
-    a.blk_count = L->blk_count;
-    a.blk_pairs = L->blk_pairs;
-    a.rescore_bph = geo.blocks_per_head;
-    a.stat_pairs = L->stat_pairs;
-    a.stat_nrr = L->stat_nrr;
-    a.pairs_out = pairs;
-    a.nrr_out = n_rerouted;
-    a.ids_out = L->ids;
-    a.seed_bound = L->seed_bound;
-    a.seed_rmax = L->seed_rmax;
-    const int rt = rr::route_tile_rows(c.k + c.m);
-    const int max_tiles = c.n_heads * ((c.n_q + rt - 1) / rt);
-    const int grid8 = (max_tiles + 7) & ~7;  // a multiple of 8: per-XCD tile ranges
-    const int grid = grid8 < 1024 ? grid8 : 1024;
-    e = timed(RR_KERNEL_REROUTE, stream, [&] { return rr::launch_route(a, c.dtype, grid, stream); });
-    if (e != hipSuccess) return hip_fail(e, "reroute launch");
+        rr::RouteArgs a = route_args(c, Qc, Kc);
+        a.layer = layer;
+        a.mode = rr::MODE_REROUTE;
+        a.led_routes = L->routes;
+        a.led_sent = L->sent;
+        a.led_build = L->build;
+        a.led_age = L->age;
+        a.flags = L->flags;
+        a.blk_count = L->blk_count;
+        a.blk_pairs = L->blk_pairs;
+        a.rescore_bph = geo.blocks_per_head;
+        a.stat_pairs = L->stat_pairs;
+        a.stat_nrr = L->stat_nrr;
+        a.pairs_out = pairs;
+        a.nrr_out = n_rerouted;
+        a.seed_bound = L->seed_bound;
+        a.seed_rmax = L->seed_rmax;
+        const int rt = rr::route_tile_rows(c.k + c.m);
+        const int max_tiles = c.n_heads * ((c.n_q + rt - 1) / rt);
+        const int grid8 = (max_tiles + 7) & ~7;  // a multiple of 8: per-XCD tile ranges
+        const int grid = grid8 < 1024 ? grid8 : 1024;
+        e = timed(RR_KERNEL_REROUTE, stream, [&] { return rr::launch_route(a, c.dtype, grid, stream); });
+        if (e != hipSuccess) return hip_fail(e, "reroute launch");
+    }
     if (routes) {
-        e = hipMemcpyAsync(routes, L->routes, sizeof(int32_t) * L->rows * c.k, hipMemcpyDeviceToDevice, stream);
+        hipError_t e = hipMemcpyAsync(routes, L->routes, sizeof(int32_t) * L->rows * c.k, hipMemcpyDeviceToDevice, stream);
         if (e != hipSuccess) return hip_fail(e, "route copy");
     }
     L->last_layer = layer;
@@ -447,8 +522,11 @@ rr_status rr_ledger_relay_stats(const rr_ledger *L, float *alpha, float *beta, i
     hipError_t e = hipSuccess;
     if (alpha) e = hipMemcpyAsync(alpha, L->alpha, sizeof(float) * L->rows, hipMemcpyDeviceToDevice, s);
     if (e == hipSuccess && beta) e = hipMemcpyAsync(beta, L->beta, sizeof(float) * L->rows, hipMemcpyDeviceToDevice, s);
-    if (e == hipSuccess && ids) e = hipMemcpyAsync(ids, L->ids, sizeof(int32_t) * L->rows, hipMemcpyDeviceToDevice, s);
-    return e == hipSuccess ? RR_OK : hip_fail(e, "relay stats copy");
+    if (e == hipSuccess && ids) {
+        hipLaunchKernelGGL(flagged_ids_kernel, dim3(L->cfg.n_heads), dim3(kIdsThreads), 0, s, L->flags, L->cfg.n_q, ids);
+        e = hipGetLastError();
+    }
+    return e == hipSuccess ? RR_OK : hip_fail(e, "relay stats");
 }
 
 rr_status rr_profile_start(void)
@@ -465,8 +543,8 @@ rr_status rr_profile_start(void)
 rr_status rr_profile_stop(double *total_ms, int64_t *launches)
 {
     g_prof.on = false;
-    double ms[RR_KERNEL_KINDS] = {0, 0, 0, 0};
-    int64_t n[RR_KERNEL_KINDS] = {0, 0, 0, 0};
+    double ms[RR_KERNEL_KINDS] = {};
+    int64_t n[RR_KERNEL_KINDS] = {};
     rr_status st = RR_OK;
     for (ProfRecord &r : g_prof.records) {
         hipError_t e = hipEventSynchronize(r.stop);

@@ -11,6 +11,8 @@ enum RouteMode : int32_t {
     MODE_FULL = 0,     // stateless routing, k slots, no sentinels
     MODE_ANCHOR = 1,   // every row: route + near-miss + random sentinels -> ledger
     MODE_REROUTE = 2,  // flagged rows only (compacted per head) -> ledger
+    MODE_RELAY = 3,    // every row rescored against the ledger on the tile's own
+                       // scores, then the flagged rows routed -> ledger
 };
 
 constexpr int kNarrowTileRows = 128;  // route tile rows when k + m <= 64
@@ -33,17 +35,22 @@ struct RouteArgs {
     int32_t *led_sent;
     int32_t *led_build;
     int32_t *led_age;
-    const uint8_t *flags;      // reroute: [rows]
-    const int32_t *blk_count;  // reroute: flagged rows per rescoring workgroup, head-major
-    const int64_t *blk_pairs;  // reroute: score pairs per rescoring workgroup, head-major
+    uint8_t *flags;            // reroute: [rows] (relay: written)
+    int32_t *blk_count;        // reroute: flagged rows per rescoring workgroup, head-major (relay: per tile)
+    int64_t *blk_pairs;        // reroute: score pairs per rescoring workgroup, head-major (relay: per tile)
     int32_t rescore_bph;       // reroute: rescoring workgroups per head
     int32_t lds_tiles;         // reroute: LDS byte offset of the per-head tile table (set by the launcher)
     int64_t *stat_pairs;       // reroute: the call's score pairs (ledger copy)
     int32_t *stat_nrr;         // reroute: the call's rerouted rows (ledger copy)
     int32_t *nrr_out;          // reroute: optional device scalar
-    int32_t *ids_out;          // reroute: compacted row ids per head, or null
     const float *seed_bound;   // reroute, or null: per row, a lower bound of its T-th score ...
     const float *seed_rmax;    // ... and its largest score, from the rescoring pass (no threshold sweep)
+    uint8_t *mask_out;         // relay: [rows] caller mask or null
+    float *alpha_out;          // relay: [rows] min over R of the rescored scores
+    float *beta_out;           // relay: [rows] max over C
+    float gamma;               // relay: guard margin
+    int32_t bm_words;          // relay: ledger bitmap row stride in (R, C) word pairs
+    uint32_t *done;            // relay: finished-workgroup counter (0 between launches)
     int64_t *pairs_out;        // optional device scalar
     int64_t pairs_value;       // value written to pairs_out (full / anchor; reroute: the workgroup sums)
 };
@@ -52,6 +59,8 @@ struct RouteArgs {
 // Supported (dtype, d) combinations; dtype 0 = binary32, 1 = bf16.
 bool route_supported(int dtype, int d, int T);
 int route_tile_rows(int T);  // query rows per route tile for T = k + m
+// Largest ledger bitmap (word pairs per row) a relay tile holds in LDS.
+int route_relay_max_bm_words(int dtype, int d, int T);
 hipError_t launch_route(const RouteArgs &a, int dtype, int grid, hipStream_t stream);
 
 }  // namespace rr

@@ -1,6 +1,6 @@
-// Dispatch of the GEMM + TopK route kernel (rr_route_impl.hpp) by input type
-// and tile width.
-#include "rr_internal.hpp"
+// Dispatch of the GEMM + TopK route kernel (rr_route_impl.hpp) by mode, input
+// type and tile width.
+#include "rr_route_impl.hpp"
 
 namespace rr {
 
@@ -10,6 +10,8 @@ hipError_t launch_route_f32_reroute(const RouteArgs &a, int grid, hipStream_t st
 hipError_t launch_route_bf16_full(const RouteArgs &a, int grid, hipStream_t stream);
 hipError_t launch_route_bf16_anchor(const RouteArgs &a, int grid, hipStream_t stream);
 hipError_t launch_route_bf16_reroute(const RouteArgs &a, int grid, hipStream_t stream);
+hipError_t launch_route_f32_relay(const RouteArgs &a, int grid, hipStream_t stream);
+hipError_t launch_route_bf16_relay(const RouteArgs &a, int grid, hipStream_t stream);
 
 bool route_supported(int dtype, int d, int T)
 {
@@ -21,6 +23,18 @@ bool route_supported(int dtype, int d, int T)
 
 int route_tile_rows(int T) { return T > 64 ? kWideTileRows : kNarrowTileRows; }
 
+int route_relay_max_bm_words(int dtype, int d, int T)
+{
+    using route_detail::relay_max_bm_words;
+    switch (d) {
+    case 32: return dtype == 0 ? relay_max_bm_words<float, 32>(T) : relay_max_bm_words<bf16_t, 32>(T);
+    case 64: return dtype == 0 ? relay_max_bm_words<float, 64>(T) : relay_max_bm_words<bf16_t, 64>(T);
+    case 128: return dtype == 0 ? relay_max_bm_words<float, 128>(T) : relay_max_bm_words<bf16_t, 128>(T);
+    case 256: return dtype == 0 ? 0 : relay_max_bm_words<bf16_t, 256>(T);
+    default: return 0;
+    }
+}
+
 hipError_t launch_route(const RouteArgs &a, int dtype, int grid, hipStream_t stream)
 {
     switch (a.mode) {
@@ -29,6 +43,8 @@ hipError_t launch_route(const RouteArgs &a, int dtype, int grid, hipStream_t str
         return dtype == 0 ? launch_route_f32_anchor(a, grid, stream) : launch_route_bf16_anchor(a, grid, stream);
     case MODE_REROUTE:
         return dtype == 0 ? launch_route_f32_reroute(a, grid, stream) : launch_route_bf16_reroute(a, grid, stream);
+    case MODE_RELAY:
+        return dtype == 0 ? launch_route_f32_relay(a, grid, stream) : launch_route_bf16_relay(a, grid, stream);
     default: break;
     }
     return hipErrorInvalidValue;

@@ -179,6 +179,8 @@ __device__ __forceinline__ void top_insert(float (&top)[TT], float x)
 
 template <typename DT, int D, int NW, int KS, int TT, int NETW, int CAPQ>
 struct RT {
+    using DType = DT;
+    static constexpr int DIM = D, NW_ = NW, KS_ = KS, TT_ = TT, CAPQ_ = CAPQ;
     static constexpr int NWV = NW * KS;            // waves
     static constexpr int NT = 64 * NWV;            // threads
     static constexpr int BM = 32 * NW;             // rows per tile
@@ -440,6 +442,48 @@ struct TopEpi {
     }
 };
 
+// Relay threshold-sweep epilogue: TopEpi's kept scores, and the rescoring
+// of the ledger's candidates on the same scores (Sec. 3.2 Eq. (6)-(7)):
+// amin = min over the routed set R, bmax = max over the sentinel set C, from
+// the row's ledger bitmaps ((R word, C word) per 32 keys): a score outside
+// the set becomes +inf for the minimum, -inf for the maximum.
+template <int TT>
+struct RelayEpi {
+    float top[16][TT];
+    int nrow;   // valid keys of the lane's row (0: padding row)
+    int sbase;  // first key of the lane's segment
+    float amin, bmax;
+    const uint2 *bmr;  // this lane's row bitmap
+
+    template <class F>
+    __device__ __forceinline__ void step(int st, const f32x16_t &acc, f32x16_t &next, const F &fq, const F &fk,
+                                         bool full)
+    {
+        const int k0 = sbase + 16 * st;  // this lane's keys: k0 .. k0 + 15 (k0 % 16 == 0)
+        const uint2 wv = bmr[k0 >> 5];
+        next = tile_product(fq, fk);
+        const uint32_t sh = (uint32_t)(k0 & 16);
+        const uint32_t mr = wv.x >> sh, mc = wv.y >> sh;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const uint32_t xb = __float_as_uint(acc[i]);
+            const uint32_t nr = (uint32_t)((int32_t)(mr << (31 - i)) >> 31);  // all-ones where in R
+            const uint32_t nc = (uint32_t)((int32_t)(mc << (31 - i)) >> 31);  // all-ones where in C
+            amin = fminf(amin, __uint_as_float((xb & nr) | (0x7F800000u & ~nr)));
+            bmax = fmaxf(bmax, __uint_as_float((xb & nc) | (0xFF800000u & ~nc)));
+        }
+        if (full) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) top_insert<TT>(top[i], acc[i]);
+        } else {
+            const int vlim = nrow - k0;  // keys k0 + i are valid for i < vlim
+#pragma unroll
+            for (int i = 0; i < 16; ++i) top_insert<TT>(top[i], (i < vlim) ? acc[i] : -INFINITY);
+        }
+        interleave_mfma<F::NS, (16 * (TT + 6) + F::NS - 1) / F::NS>();
+    }
+};
+
 // The lane's 16 x TT kept scores -> its segment's part of the row's kept
 // set in LDS (rows of UST floats).
 template <class C, int TT>
@@ -583,6 +627,9 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
     __shared__ int32_t s_head, s_ncols, s_wave[C::NWV];
     __shared__ unsigned long long s_tot_pairs;
     __shared__ int32_t s_tot_rows;
+    __shared__ float r_amin[KS][BM], r_bmax[KS][BM];  // relay: per key split, alpha / beta of a row
+    __shared__ int32_t r_nc[BM], r_ns[BM];            // relay: the row's ledger counts |R|, |C|
+    __shared__ int32_t s_last;
 
     const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
     const int rb = w % NW, p = w / NW;  // row block and key split of this wave
@@ -591,7 +638,8 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
     const int group = a.n_heads / a.n_kv_heads;
     const int c_sent = a.m + a.r;
 
-    if (a.pairs_out && mode != MODE_REROUTE && blockIdx.x == 0 && tid == 0) *a.pairs_out = a.pairs_value;
+    if (a.pairs_out && (mode == MODE_FULL || mode == MODE_ANCHOR) && blockIdx.x == 0 && tid == 0)
+        *a.pairs_out = a.pairs_value;
 
     // Reroute: the per-head tile table (heads in XCD-major order) from the
     // rescoring workgroups' flagged-row counts; workgroup 0 also publishes the
@@ -705,7 +753,6 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
                 if (f && rank >= lo && rank < hi) {
                     row_i[rank - lo] = i;
                     row_g[rank - lo] = h * a.n_q + i;
-                    if (a.ids_out) a.ids_out[(int64_t)h * a.n_q + rank] = i;
                 }
                 run += tot;
                 __syncthreads();
@@ -745,6 +792,58 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
             (minn == INT_MAX) ? nb : (slack < 0 ? 0 : min(nb, slack / 16 + 1)));
         const unsigned char *Kg =
             reinterpret_cast<const unsigned char *>(a.K) + (int64_t)(h / group) * a.n_k * C::ROWB;
+        // relay: the ledger rows -> per-row bitmaps over the key range, (R
+        // word, C word) per 32 keys, in the candidate region (free until the
+        // collection sweep).  Wave w reads rows w, w + NWV, ..., a lane per
+        // ledger slot; every lane loads (masked slots read row 0).
+        uint2 *rbm = reinterpret_cast<uint2 *>(ss);
+        if constexpr (mode == MODE_RELAY) {
+            const int nwd = a.bm_words;
+            for (int j = tid; j < BM * nwd; j += C::NT) rbm[j] = make_uint2(0u, 0u);
+            if (tid == 0) {
+                s_tot_pairs = 0ull;
+                s_tot_rows = 0;
+            }
+            lds_barrier();
+            constexpr int RPW = BM / C::NWV;
+            static_assert(BM % C::NWV == 0, "rows split evenly over the waves");
+            int nc[RPW], ns[RPW];
+#pragma unroll
+            for (int q = 0; q < RPW; ++q) nc[q] = ns[q] = 0;
+            uint32_t *bw = reinterpret_cast<uint32_t *>(rbm);
+            const int c_led = a.k + c_sent;
+            for (int s0 = 0; s0 < c_led; s0 += 64) {
+                const int slot = s0 + lane;
+                const bool inr = slot < a.k, live = slot < c_led;
+                const int32_t *col = inr ? a.led_routes + slot : (live ? a.led_sent + (slot - a.k) : a.led_routes);
+                const int64_t stride = inr ? a.k : (live ? c_sent : a.k);
+                int id[RPW];
+#pragma unroll
+                for (int q = 0; q < RPW; ++q) {
+                    const int64_t g = row_g[w + q * C::NWV];
+                    const bool ok = live && g >= 0;
+                    const int v = col[(ok ? g : 0) * stride];
+                    id[q] = ok ? v : -1;
+                }
+#pragma unroll
+                for (int q = 0; q < RPW; ++q) {
+                    const int r = w + q * C::NWV;
+                    const bool ok = id[q] >= 0 && id[q] < a.n_k;  // ledger ids lie in [0, n_i); -1 is an empty slot
+                    if (ok) atomicOr(&bw[2 * (r * nwd + (id[q] >> 5)) + (inr ? 0 : 1)], 1u << (id[q] & 31));
+                    nc[q] += __popcll(__ballot(ok && inr));
+                    ns[q] += __popcll(__ballot(ok && !inr));
+                }
+            }
+            if (lane == 0) {
+#pragma unroll
+                for (int q = 0; q < RPW; ++q) {
+                    r_nc[w + q * C::NWV] = nc[q];
+                    r_ns[w + q * C::NWV] = ns[q];
+                }
+            }
+            lds_barrier();
+        }
+
         Frag<DT, D> fq;
         if (row_g[myrow] >= 0)
             fq.load(reinterpret_cast<const DT *>(a.Q) + (int64_t)row_g[myrow] * D, hh);
@@ -769,6 +868,32 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
                 b1_s[tid] = b;
                 rmax_s[tid] = x;
             }
+        } else if constexpr (mode == MODE_RELAY) {
+            {
+                RelayEpi<TT> epi;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+#pragma unroll
+                    for (int j = 0; j < TT; ++j) epi.top[i][j] = -INFINITY;
+                }
+                epi.nrow = nrow;
+                epi.sbase = sbase;
+                epi.amin = INFINITY;
+                epi.bmax = -INFINITY;
+                epi.bmr = rbm + myrow * a.bm_words;
+                sweep_keys<DT, D, C>(fq, Kg, a.n_k, seg, nb, full_stages, tid, p, hh, l32, bt, epi);
+                // the row's lanes: halves hh of a wave here, key splits p below
+                const float am = fminf(epi.amin, __shfl_xor(epi.amin, 32, 64));
+                const float bx = fmaxf(epi.bmax, __shfl_xor(epi.bmax, 32, 64));
+                if (hh == 0) {
+                    r_amin[p][myrow] = am;
+                    r_bmax[p][myrow] = bx;
+                }
+                __syncthreads();  // every wave is done with the key tiles and the bitmaps
+                store_kept<C, TT>(us, myrow, myseg, epi.top);
+            }
+            __syncthreads();
+            bound_of_kept<C>(us, tid, T, b1_s, rmax_s);
         } else {
             {
                 TopEpi<TT> epi;
@@ -787,6 +912,94 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
             bound_of_kept<C>(us, tid, T, b1_s, rmax_s);
         }
         __syncthreads();
+
+        if constexpr (mode == MODE_RELAY) {
+            // the trigger (Eq. (8)): a row keeps its route unless C is
+            // non-empty and beta + gamma >= alpha.  Kept rows are finished
+            // (outputs and age); the rest of the tile routes the flagged rows
+            // only, the others now count as padding.  Score pairs follow the
+            // method's accounting: the ledger's candidates, plus n_i for each
+            // refreshed row.
+            unsigned long long pr = 0;
+            int cf = 0;
+            if (tid < BM && row_g[tid] >= 0) {
+                const int64_t row = row_g[tid];
+                float al = r_amin[0][tid], be = r_bmax[0][tid];
+#pragma unroll
+                for (int q = 1; q < KS; ++q) {
+                    al = fminf(al, r_amin[q][tid]);
+                    be = fmaxf(be, r_bmax[q][tid]);
+                }
+                const int ncr = r_nc[tid], nsr = r_ns[tid];
+                const bool flag = nsr > 0 && (be + a.gamma >= al);
+                a.flags[row] = flag ? 1 : 0;
+                if (a.mask_out) a.mask_out[row] = flag ? 1 : 0;
+                a.alpha_out[row] = al;
+                a.beta_out[row] = be;
+                if (!flag) {
+                    a.led_age[row] = a.layer - a.led_build[row];
+                    row_g[tid] = -1;
+                }
+                pr = (unsigned long long)(ncr + nsr + (flag ? row_n[tid] : 0));
+                cf = flag ? 1 : 0;
+            }
+            if (tid < ((BM + 63) & ~63)) {
+#pragma unroll
+                for (int off = 32; off > 0; off >>= 1) {
+                    pr += (unsigned long long)__shfl_xor((long long)pr, off, 64);
+                    cf += __shfl_xor(cf, off, 64);
+                }
+                if (lane == 0) {
+                    atomicAdd(&s_tot_pairs, pr);
+                    atomicAdd(&s_tot_rows, cf);
+                }
+            }
+            __syncthreads();
+            const int tile_flagged = s_tot_rows;
+            // the launch's totals: each workgroup publishes its tile's counts
+            // and the last one to finish sums them (every relay tile holds a
+            // row, so every workgroup gets here exactly once)
+            if (tid == 0) {
+                a.blk_pairs[blockIdx.x] = (int64_t)s_tot_pairs;
+                a.blk_count[blockIdx.x] = s_tot_rows;
+                __threadfence();
+                s_last = (atomicAdd(a.done, 1u) == gridDim.x - 1) ? 1 : 0;
+            }
+            __syncthreads();
+            if (s_last) {
+                __threadfence();
+                if (tid == 0) {
+                    s_tot_pairs = 0ull;
+                    s_tot_rows = 0;
+                }
+                __syncthreads();
+                unsigned long long pp = 0;
+                int cc = 0;
+                for (int j = tid; j < (int)gridDim.x; j += C::NT) {
+                    pp += (unsigned long long)__hip_atomic_load(&a.blk_pairs[j], __ATOMIC_RELAXED,
+                                                                __HIP_MEMORY_SCOPE_AGENT);
+                    cc += __hip_atomic_load(&a.blk_count[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+#pragma unroll
+                for (int off = 32; off > 0; off >>= 1) {
+                    pp += (unsigned long long)__shfl_xor((long long)pp, off, 64);
+                    cc += __shfl_xor(cc, off, 64);
+                }
+                if (lane == 0) {
+                    atomicAdd(&s_tot_pairs, pp);
+                    atomicAdd(&s_tot_rows, cc);
+                }
+                __syncthreads();
+                if (tid == 0) {
+                    *a.stat_pairs = (int64_t)s_tot_pairs;
+                    *a.stat_nrr = s_tot_rows;
+                    if (a.pairs_out) *a.pairs_out = (int64_t)s_tot_pairs;
+                    if (a.nrr_out) *a.nrr_out = s_tot_rows;
+                    __hip_atomic_store(a.done, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
+            if (tile_flagged == 0) continue;  // (uniform) nothing to route in this tile
+        }
         if (tid < BM) {
             const bool real = row_g[tid] >= 0;
             th_s[tid] = real ? b1_s[tid] : INFINITY;  // padding rows collect nothing
@@ -1273,6 +1486,8 @@ hipError_t launch_t(RouteArgs a, int grid, hipStream_t stream)
     static_assert((size_t)C::BM * C::UST * 4 <=
                       (size_t)C::BM * (NETW + 1) * 4 + (size_t)C::BM * C::SS * 4 + (size_t)C::BM * C::SI * 2,
                   "the kept scores of the threshold sweep fit the dynamic region");
+    if (MODE == MODE_RELAY && (size_t)a.bm_words * 8 > (size_t)C::SS * 4 + (size_t)C::SI * 2)
+        return hipErrorInvalidValue;  // the ledger bitmaps exceed the candidate region
     if (MODE == MODE_REROUTE) {  // the per-head tile table
         lds = (lds + 15) & ~(size_t)15;
         a.lds_tiles = (int32_t)lds;
@@ -1291,13 +1506,33 @@ hipError_t launch_t(RouteArgs a, int grid, hipStream_t stream)
 // T = k + m <= 64: 128-row tiles, 8 waves (two key splits), top-2 per slot, a
 // 64-entry network; T <= 128: 64-row tiles, 4 waves, top-3, a 128-entry
 // network.  The sub-list share CAPQ keeps the workgroup's LDS within 160 KB.
+template <typename DT, int D>
+using NarrowRT = RT<DT, D, 4, 2, 2, 64, (D * (int)sizeof(DT) <= 256 ? 32 : 20)>;
+template <typename DT, int D>
+using WideRT = RT<DT, D, 2, 2, 3, 128, (D * (int)sizeof(DT) <= 256 ? 48 : 32)>;
+
+template <int MODE, class C>
+hipError_t launch_c(const RouteArgs &a, int grid, hipStream_t stream)
+{
+    return launch_t<MODE, typename C::DType, C::DIM, C::NW_, C::KS_, C::TT_, C::NET, C::CAPQ_>(a, grid, stream);
+}
+
 template <int MODE, typename DT, int D>
 hipError_t launch_d(const RouteArgs &a, int grid, hipStream_t stream)
 {
-    static_assert(kWideTileRows == 64 && kNarrowTileRows == 128, "tile heights of the two classes");
-    constexpr int ROWB = D * (int)sizeof(DT);
-    if (a.k + a.m > 64) return launch_t<MODE, DT, D, 2, 2, 3, 128, (ROWB <= 256 ? 48 : 32)>(a, grid, stream);
-    return launch_t<MODE, DT, D, 4, 2, 2, 64, (ROWB <= 256 ? 32 : 20)>(a, grid, stream);
+    static_assert(WideRT<DT, D>::BM == kWideTileRows && NarrowRT<DT, D>::BM == kNarrowTileRows,
+                  "tile heights of the two classes");
+    if (a.k + a.m > 64) return launch_c<MODE, WideRT<DT, D>>(a, grid, stream);
+    return launch_c<MODE, NarrowRT<DT, D>>(a, grid, stream);
+}
+
+// Ledger bitmap words (R, C pairs per row) that a relay tile's candidate
+// region holds.
+template <typename DT, int D>
+int relay_max_bm_words(int T)
+{
+    if (T > 64) return (WideRT<DT, D>::SS * 4 + WideRT<DT, D>::SI * 2) / 8;
+    return (NarrowRT<DT, D>::SS * 4 + NarrowRT<DT, D>::SI * 2) / 8;
 }
 
 template <int MODE, typename DT>

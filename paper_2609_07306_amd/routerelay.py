@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_HERE, "librouterelay.so")
 
 RR_OK, RR_ERR_INVALID, RR_ERR_OOM, RR_ERR_HIP, RR_ERR_STATE, RR_ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 RR_F32, RR_BF16 = 0, 1
+RR_OPT_SPLIT_RELAY, RR_OPT_ONE_PASS_RELAY = 1, 2
 
 EXPORTED = (
     "rr_ledger_create", "rr_ledger_destroy", "rr_anchor_route", "rr_relay_layer", "rr_full_route",
@@ -25,7 +26,7 @@ EXPORTED = (
     "rr_ledger_index_bytes", "rr_status_string", "rr_last_error", "rr_profile_start",
     "rr_profile_stop",
 )
-KERNEL_KINDS = ("full", "anchor", "reroute", "rescore")
+KERNEL_KINDS = ("full", "anchor", "reroute", "rescore", "relay")
 
 
 class RRError(RuntimeError):
@@ -39,7 +40,7 @@ class _Config(ctypes.Structure):
         ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("n_q", ctypes.c_int32),
         ("n_k", ctypes.c_int32), ("d", ctypes.c_int32), ("k", ctypes.c_int32), ("m", ctypes.c_int32),
         ("r", ctypes.c_int32), ("dtype", ctypes.c_int32), ("causal", ctypes.c_int32),
-        ("gamma", ctypes.c_float), ("reserved", ctypes.c_uint32), ("seed", ctypes.c_uint64),
+        ("gamma", ctypes.c_float), ("options", ctypes.c_uint32), ("seed", ctypes.c_uint64),
     ]
 
 
@@ -79,6 +80,9 @@ def _check(status: int):
         raise RRError(status, lib.rr_last_error().decode())
 
 
+_RELAY_OPTIONS = {"auto": 0, "split": RR_OPT_SPLIT_RELAY, "one_pass": RR_OPT_ONE_PASS_RELAY}
+
+
 @dataclass(frozen=True)
 class Config:
     """Shape and rule parameters (rr_config)."""
@@ -94,6 +98,7 @@ class Config:
     causal: bool = False
     gamma: float = 0.0
     seed: int = 0
+    relay: str = "auto"  # relay schedule: "auto" | "one_pass" | "split" (rr_option)
 
     @property
     def rows(self) -> int:
@@ -102,7 +107,8 @@ class Config:
     def c(self) -> _Config:
         return _Config(self.n_heads, self.n_kv_heads, self.n_q, self.n_k, self.d, self.k, self.m,
                        self.r, RR_BF16 if self.dtype == "bf16" else RR_F32, int(self.causal),
-                       float(self.gamma), 0, int(self.seed) & 0xFFFFFFFFFFFFFFFF)
+                       float(self.gamma), _RELAY_OPTIONS[self.relay],
+                       int(self.seed) & 0xFFFFFFFFFFFFFFFF)
 
     @staticmethod
     def of(w) -> "Config":
@@ -150,8 +156,8 @@ def profile_start():
 
 def profile_stop():
     """Stop profiling; returns {kind: (total_ms, launches)}."""
-    ms = (ctypes.c_double * 4)()
-    n = (ctypes.c_int64 * 4)()
+    ms = (ctypes.c_double * len(KERNEL_KINDS))()
+    n = (ctypes.c_int64 * len(KERNEL_KINDS))()
     _check(lib.rr_profile_stop(ms, n))
     return {k: (ms[i], n[i]) for i, k in enumerate(KERNEL_KINDS)}
 

@@ -75,15 +75,16 @@ def n_valid_rows(p):
     return np.minimum(i + 1, p.n_k) if p.causal else np.full(p.rows, p.n_k)
 
 
-def rollout_compare(w, gamma=None, check_scores=True):
-    """Runs the workload's anchor/relay schedule on the GPU and on the oracle.
+def rollout_compare(w, gamma=None, check_scores=True, relay="auto"):
+    """Runs the workload's anchor/relay schedule on the GPU and on the oracle
+    (relay: the relay schedule, "auto", "one_pass" or "split").
 
     Returns a dict of statistics; raises AssertionError on any mismatch of a
     trusted row."""
     if gamma is not None:
         w = w.with_(gamma=gamma)
     p = problem_of(w)
-    cfg = rr.Config.of(w)
+    cfg = dataclasses.replace(rr.Config.of(w), relay=relay)
     L = rr.Ledger(cfg)
     ref = oracle.new_ledger(p)
     trusted = np.zeros(p.rows, dtype=bool)
@@ -127,9 +128,15 @@ def rollout_compare(w, gamma=None, check_scores=True):
             if np.array_equal(gmask, omask) and trusted.all():
                 assert int(pairs_t.item()) == out["pairs"]
             if check_scores:
-                alpha, beta, _ = L.relay_stats()
+                alpha, beta, ids = L.relay_stats()
                 torch.cuda.synchronize()
                 alpha, beta = alpha.cpu().numpy(), beta.cpu().numpy()
+                # the rerouted rows of each head, ascending, then -1
+                ids = ids.cpu().numpy().reshape(p.n_heads, p.n_q)
+                for h in range(p.n_heads):
+                    fl = np.flatnonzero(gmask.reshape(p.n_heads, p.n_q)[h])
+                    np.testing.assert_array_equal(ids[h, :len(fl)], fl)
+                    assert np.all(ids[h, len(fl):] == -1)
                 tol = TOL[w.dtype]
                 ok = trusted
                 assert np.all(np.abs(alpha[ok] - out["alpha"][ok]) <= tol * out["alpha_abs"][ok] + 1e-30)

@@ -78,6 +78,29 @@ def test_invalid_configs_rejected_before_any_launch(kw, status):
         assert got == status
 
 
+@pytest.mark.parametrize("options", [3, 4, 0x80000000])
+def test_invalid_options_rejected(options):
+    """rr_config.options: the two relay schedules exclude each other; other
+    bits are unknown."""
+    rr = _rr()
+    c = _cfg().c()
+    c.options = options
+    h = ctypes.c_void_p()
+    assert rr.lib.rr_ledger_create(ctypes.byref(c), ctypes.byref(h)) == -1
+    assert not h.value
+
+
+def test_kernel_kinds_match_binding():
+    """The binding sizes its profile arrays from the header's kernel kinds."""
+    rr = _rr()
+    src = open(HEADER).read()
+    kinds = dict((n, int(v)) for n, v in re.findall(r"RR_KERNEL_([A-Z]+)\s*=\s*(\d+)", src))
+    n = kinds.pop("KINDS")
+    assert len(rr.KERNEL_KINDS) == n
+    for name, v in kinds.items():
+        assert rr.KERNEL_KINDS[v] == name.lower()
+
+
 def test_null_arguments():
     rr = _rr()
     assert rr.lib.rr_ledger_destroy(None) == 0
