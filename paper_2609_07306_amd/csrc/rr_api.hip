@@ -207,8 +207,8 @@ rr::RouteArgs route_args(const rr_config &c, const void *Q, const void *K)
     a.m = c.m;
     a.r = c.r;
     a.causal = c.causal;
-    const int tr = rr::route_tile_rows(c.k + c.m);
-    a.tiles_per_head = (c.n_q + tr - 1) / tr;
+    a.tile_rows = rr::route_tile_rows(c.k + c.m, c.n_heads, c.n_q);
+    a.tiles_per_head = (c.n_q + a.tile_rows - 1) / a.tile_rows;
     a.seed = c.seed;
     return a;
 }
@@ -438,8 +438,7 @@ rr_status rr_relay_layer(rr_ledger *L, int32_t layer, const void *Qc, const void
         a.nrr_out = n_rerouted;
         a.seed_bound = L->seed_bound;
         a.seed_rmax = L->seed_rmax;
-        const int rt = rr::route_tile_rows(c.k + c.m);
-        const int max_tiles = c.n_heads * ((c.n_q + rt - 1) / rt);
+        const int max_tiles = c.n_heads * a.tiles_per_head;
         const int grid8 = (max_tiles + 7) & ~7;  // a multiple of 8: per-XCD tile ranges
         const int grid = grid8 < 1024 ? grid8 : 1024;
         e = timed(RR_KERNEL_REROUTE, stream, [&] { return rr::launch_route(a, c.dtype, grid, stream); });

@@ -17,6 +17,8 @@ enum RouteMode : int32_t {
 
 constexpr int kNarrowTileRows = 128;  // route tile rows when k + m <= 64
 constexpr int kWideTileRows = 64;     // route tile rows when 64 < k + m <= 128
+constexpr int kSmallTileRows = 32;    // route tile rows when k + m <= 64 and 128-row tiles would be few
+constexpr int kFewTiles = 64;         // ... fewer than this many (a quarter of the compute units)
 
 struct RouteArgs {
     const void *Q;
@@ -26,6 +28,7 @@ struct RouteArgs {
     int32_t causal;
     int32_t layer;
     int32_t mode;
+    int32_t tile_rows;       // route_tile_rows() of the call's shape
     int32_t tiles_per_head;  // ceil(n_q / tile rows) for full / anchor tiles
     int32_t lds_region0;     // set by the launcher: bytes of the key-tile region
     uint64_t seed;
@@ -58,7 +61,7 @@ struct RouteArgs {
 
 // Supported (dtype, d) combinations; dtype 0 = binary32, 1 = bf16.
 bool route_supported(int dtype, int d, int T);
-int route_tile_rows(int T);  // query rows per route tile for T = k + m
+int route_tile_rows(int T, int n_heads, int n_q);  // query rows per route tile for T = k + m
 // Largest ledger bitmap (word pairs per row) a relay tile holds in LDS.
 int route_relay_max_bm_words(int dtype, int d, int T);
 hipError_t launch_route(const RouteArgs &a, int dtype, int grid, hipStream_t stream);

@@ -21,7 +21,15 @@ bool route_supported(int dtype, int d, int T)
     return false;
 }
 
-int route_tile_rows(int T) { return T > 64 ? kWideTileRows : kNarrowTileRows; }
+// Few 128-row tiles leave most compute units idle and each tile's sweeps
+// long (binary32 products run at 1/16 of the bf16 rate): 32-row tiles then
+// spread the same rows over four times the workgroups.
+int route_tile_rows(int T, int n_heads, int n_q)
+{
+    if (T > 64) return kWideTileRows;
+    const int64_t narrow = (int64_t)n_heads * ((n_q + kNarrowTileRows - 1) / kNarrowTileRows);
+    return narrow < kFewTiles ? kSmallTileRows : kNarrowTileRows;
+}
 
 int route_relay_max_bm_words(int dtype, int d, int T)
 {

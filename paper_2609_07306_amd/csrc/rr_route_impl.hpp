@@ -1510,6 +1510,8 @@ template <typename DT, int D>
 using NarrowRT = RT<DT, D, 4, 2, 2, 64, (D * (int)sizeof(DT) <= 256 ? 32 : 20)>;
 template <typename DT, int D>
 using WideRT = RT<DT, D, 2, 2, 3, 128, (D * (int)sizeof(DT) <= 256 ? 48 : 32)>;
+template <typename DT, int D>
+using SmallRT = RT<DT, D, 1, 2, 2, 64, (D * (int)sizeof(DT) <= 256 ? 32 : 20)>;
 
 template <int MODE, class C>
 hipError_t launch_c(const RouteArgs &a, int grid, hipStream_t stream)
@@ -1520,9 +1522,13 @@ hipError_t launch_c(const RouteArgs &a, int grid, hipStream_t stream)
 template <int MODE, typename DT, int D>
 hipError_t launch_d(const RouteArgs &a, int grid, hipStream_t stream)
 {
-    static_assert(WideRT<DT, D>::BM == kWideTileRows && NarrowRT<DT, D>::BM == kNarrowTileRows,
-                  "tile heights of the two classes");
+    static_assert(WideRT<DT, D>::BM == kWideTileRows && NarrowRT<DT, D>::BM == kNarrowTileRows &&
+                      SmallRT<DT, D>::BM == kSmallTileRows,
+                  "tile heights of the three classes");
+    static_assert(SmallRT<DT, D>::SS == NarrowRT<DT, D>::SS && SmallRT<DT, D>::SI == NarrowRT<DT, D>::SI,
+                  "small and narrow tiles give a row the same candidate region");
     if (a.k + a.m > 64) return launch_c<MODE, WideRT<DT, D>>(a, grid, stream);
+    if (a.tile_rows == kSmallTileRows) return launch_c<MODE, SmallRT<DT, D>>(a, grid, stream);
     return launch_c<MODE, NarrowRT<DT, D>>(a, grid, stream);
 }
 
