@@ -18,7 +18,7 @@ enum RouteMode : int32_t {
 constexpr int kNarrowTileRows = 128;  // route tile rows when k + m <= 64
 constexpr int kWideTileRows = 64;     // route tile rows when 64 < k + m <= 128
 constexpr int kSmallTileRows = 32;    // route tile rows when k + m <= 64 and 128-row tiles would be few
-constexpr int kFewTiles = 64;         // ... fewer than this many (a quarter of the compute units)
+constexpr int kFewTiles = 256;        // ... fewer than this many (one per compute unit)
 
 struct RouteArgs {
     const void *Q;

@@ -21,9 +21,11 @@ bool route_supported(int dtype, int d, int T)
     return false;
 }
 
-// Few 128-row tiles leave most compute units idle and each tile's sweeps
-// long (binary32 products run at 1/16 of the bf16 rate): 32-row tiles then
-// spread the same rows over four times the workgroups.
+// Fewer 128-row tiles than compute units leave units idle and each tile's
+// sweeps long (binary32 products run at 1/16 of the bf16 rate; a causal
+// tile's key range is its last row's): 32-row tiles then spread the same
+// rows over four times the workgroups.  With a tile per unit or more, the
+// extra passes over each key head cost more than they save.
 int route_tile_rows(int T, int n_heads, int n_q)
 {
     if (T > 64) return kWideTileRows;
