@@ -403,6 +403,7 @@ rr_status rr_relay_layer(rr_ledger *L, int32_t layer, const void *Qc, const void
         rr::rescore_geometry(L->rows, c.n_q, c.n_k, geo);
         s.blocks_per_head = geo.blocks_per_head;
         s.rows_per_wave = geo.rows_per_wave;
+        s.rows_per_block = geo.rows_per_block;
         s.dense = geo.dense ? 1 : 0;
         s.bm_words = geo.bm_words;
         s.gamma = c.gamma;

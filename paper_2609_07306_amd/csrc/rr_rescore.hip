@@ -260,17 +260,21 @@ hipError_t launch_d(const RescoreArgs &a, hipStream_t stream)
 void rescore_geometry(int64_t rows, int n_q, int n_k, RescoreGeometry &g)
 {
     // dense tiles when the key range is short enough for the bitmaps and the
-    // tiles fill at least half the chip (measured: dense wins at 128 tiles of
-    // n_k = 512, the gather at 64 tiles of n_k = 256); otherwise the gather
-    const int64_t tiles = (rows / n_q) * ((n_q + rescore_dense_tile_rows() - 1) / rescore_dense_tile_rows());
-    g.dense = n_k <= kRescoreDenseMaxKeys && tiles >= kRescoreDenseMinTiles;
+    // tiles fill at least half the chip: 128-row tiles from a tile per
+    // compute unit, else 64-row tiles (measured at n_k = 512 with 128 tiles of
+    // 128 rows: 64-row tiles 19.0 us, 128-row 22.3; at n_k = 1024 with 256:
+    // 42 against 29); otherwise the gather
+    const int64_t heads = rows / n_q;
+    const int64_t large = heads * ((n_q + kDenseRowsLarge - 1) / kDenseRowsLarge);
+    const int64_t small = heads * ((n_q + kDenseRowsSmall - 1) / kDenseRowsSmall);
+    g.dense = n_k <= kRescoreDenseMaxKeys && (large >= kRescoreDenseFullTiles || small >= kRescoreDenseMinTiles);
     if (g.dense) {
-        // 128-row tiles over the whole key range; a bitmap row holds two
-        // word pairs per 64 keys of the padded range plus one, so that rows
-        // lie an odd number of pairs apart and the 32 rows a wave reads
-        // together fall in distinct LDS banks
+        // tiles over the whole key range; a bitmap row holds two word pairs
+        // per 64 keys of the padded range plus one, so that rows lie an odd
+        // number of pairs apart and the 32 rows a wave reads together fall in
+        // distinct LDS banks
         g.rows_per_wave = 0;
-        g.rows_per_block = rescore_dense_tile_rows();
+        g.rows_per_block = large >= kRescoreDenseFullTiles ? kDenseRowsLarge : kDenseRowsSmall;
         g.blocks_per_head = (n_q + g.rows_per_block - 1) / g.rows_per_block;
         g.bm_words = 2 * ((n_k + 63) / 64) + 1;
         return;

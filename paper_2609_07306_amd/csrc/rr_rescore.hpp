@@ -12,7 +12,10 @@ constexpr int kRescoreBlocks = 512;         // target rescoring workgroups per l
 constexpr int kRescoreMaxRowsPerWave = 16;  // rows a rescoring wave scores in turn
 constexpr int kRescoreLanesPerCand = 4;     // lanes sharing one candidate's dot product (4 or 8)
 constexpr int kRescoreDenseMaxKeys = 2048;  // dense (MFMA tile) rescoring up to this many key chunks
-constexpr int kRescoreDenseMinTiles = 128;  // ... and with at least this many 128-row tiles (half the CUs)
+constexpr int kDenseRowsLarge = 128;        // dense tile rows with at least kRescoreDenseFullTiles such tiles
+constexpr int kDenseRowsSmall = 64;         // ... else, with at least kRescoreDenseMinTiles of these
+constexpr int kRescoreDenseFullTiles = 256;  // a tile per compute unit
+constexpr int kRescoreDenseMinTiles = 128;   // half the compute units
 
 struct RescoreArgs {
     const void *Q;
@@ -23,6 +26,7 @@ struct RescoreArgs {
     int32_t layer;
     int32_t blocks_per_head;  // ceil(n_q / rows per block)
     int32_t rows_per_wave;    // gather: rows per block = kRescoreWaves * rows_per_wave
+    int32_t rows_per_block;   // dense: tile rows (kDenseRowsLarge or kDenseRowsSmall)
     int32_t dense;            // 1: the MFMA tile kernel (128-row tiles), 0: the gather kernel
     int32_t bm_words;         // dense: bitmap row stride in (R, C) word pairs (padded key range + 1, odd)
     float gamma;
@@ -48,7 +52,6 @@ struct RescoreGeometry {
 };
 void rescore_geometry(int64_t rows, int n_q, int n_k, RescoreGeometry &g);
 hipError_t launch_rescore(const RescoreArgs &a, int dtype, hipStream_t stream);
-int rescore_dense_tile_rows();
 bool rescore_dense_seeds(int dtype, int d);  // the dense kernel writes seed_bound / seed_rmax
 hipError_t launch_rescore_dense(const RescoreArgs &a, int dtype, hipStream_t stream);
 

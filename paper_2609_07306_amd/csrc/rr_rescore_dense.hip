@@ -3,7 +3,7 @@
 //
 // The sampled product of Eq. (5) names at most k + m + r keys per row, but
 // with n_k <= 2048 the candidates cover a few percent of a head's keys, and
-// on matrix cores the full product of a 128-row tile with all of its head's
+// on matrix cores the full product of a 64- or 128-row tile with all of its head's
 // keys costs less than gathering the candidate key rows one by one: the key
 // head streams once per tile through LDS (the routing sweep's staging), the
 // MFMAs produce every score, and the epilogue keeps a score only where the
@@ -32,11 +32,10 @@ namespace {
 
 using route_detail::RT;
 
-// Tiles of 32 * kDenseRowBlocks rows; waves = row blocks x 2 key splits.
-constexpr int kDenseRowBlocks = 4;
-constexpr int kDenseThreads = 64 * kDenseRowBlocks * 2;
-template <typename DT, int D>
-using DenseRT = RT<DT, D, kDenseRowBlocks, 2, 2, 64, 32>;
+// Tiles of 32 * NW rows (NW = 4 or 2 row blocks); waves = row blocks x 2
+// key splits.
+template <typename DT, int D, int NW>
+using DenseRT = RT<DT, D, NW, 2, 2, 64, 32>;
 // Tiles whose key fragments take at most 256 bytes per row have the
 // registers for the kept scores of the threshold step as well.
 template <typename DT, int D>
@@ -85,13 +84,13 @@ struct DenseEpi {
     }
 };
 
-template <typename DT, int D>
-__global__ __launch_bounds__(kDenseThreads) void rescore_dense_kernel(RescoreArgs a)
+template <typename DT, int D, int NW>
+__global__ __launch_bounds__(128 * NW) void rescore_dense_kernel(RescoreArgs a)
 {
-    using C = DenseRT<DT, D>;
-    static_assert(C::NT == kDenseThreads, "launch bounds of the tile shape");
+    using C = DenseRT<DT, D, NW>;
+    static_assert(C::NT == 128 * NW, "launch bounds of the tile shape");
     constexpr bool SEED = kDenseSeeds<DT, D>;
-    constexpr int BM = C::BM, NT = C::NT, NW = kDenseRowBlocks, KS = 2;
+    constexpr int BM = C::BM, NT = C::NT, KS = 2;
     constexpr int NWB = (BM + 63) / 64;  // waves holding one lane per row
     extern __shared__ __align__(16) unsigned char smem[];
     unsigned char *bt = smem;                                     // [2][KS][32][BSTR] key tiles
@@ -283,25 +282,33 @@ __global__ __launch_bounds__(kDenseThreads) void rescore_dense_kernel(RescoreArg
     }
 }
 
-template <typename DT, int D>
-hipError_t launch_d(const RescoreArgs &a, hipStream_t stream)
+template <typename DT, int D, int NW>
+hipError_t launch_n(const RescoreArgs &a, hipStream_t stream)
 {
-    using C = DenseRT<DT, D>;
+    using C = DenseRT<DT, D, NW>;
     size_t lds = (size_t)2 * C::ST + (size_t)C::BM * a.bm_words * sizeof(uint2);
     if (kDenseSeeds<DT, D>) lds = std::max(lds, (size_t)C::BM * C::UST * sizeof(float));  // the kept scores
-    const void *fn = reinterpret_cast<const void *>(&rescore_dense_kernel<DT, D>);
+    const void *fn = reinterpret_cast<const void *>(&rescore_dense_kernel<DT, D, NW>);
     if (lds > 65536) {
         const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL((rescore_dense_kernel<DT, D>), dim3(a.n_heads * a.blocks_per_head), dim3(C::NT), lds, stream,
-                       a);
+    hipLaunchKernelGGL((rescore_dense_kernel<DT, D, NW>), dim3(a.n_heads * a.blocks_per_head), dim3(C::NT), lds,
+                       stream, a);
     return hipGetLastError();
 }
 
-}  // namespace
+template <typename DT, int D>
+hipError_t launch_d(const RescoreArgs &a, hipStream_t stream)
+{
+    static_assert(DenseRT<DT, D, 4>::BM == kDenseRowsLarge && DenseRT<DT, D, 2>::BM == kDenseRowsSmall,
+                  "dense tile heights");
+    if (a.rows_per_block == kDenseRowsSmall) return launch_n<DT, D, 2>(a, stream);
+    if (a.rows_per_block == kDenseRowsLarge) return launch_n<DT, D, 4>(a, stream);
+    return hipErrorInvalidValue;
+}
 
-int rescore_dense_tile_rows() { return DenseRT<float, 32>::BM; }
+}  // namespace
 
 bool rescore_dense_seeds(int dtype, int d)
 {

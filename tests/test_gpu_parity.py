@@ -234,6 +234,10 @@ ROLLOUTS = [
     ("scale", {"n_heads": 256, "n_kv_heads": 256, "n": 128, "r": 0, "n_layers": 4, "anchor_every": 2}),
     ("scale", {"n_heads": 256, "n_kv_heads": 256, "n": 192, "k": 48, "m": 24, "r": 8, "n_layers": 4,
                "anchor_every": 2}),
+    # dense rescoring in 64-row tiles (fewer 128-row tiles than compute
+    # units), with a ragged last tile in the causal case
+    ("scale", {"n_heads": 64, "n_kv_heads": 64, "n": 256, "n_layers": 4, "anchor_every": 2}),
+    ("gqa", {"n_heads": 64, "n_kv_heads": 16, "n": 160, "n_layers": 4, "anchor_every": 2}),
 ]
 
 
@@ -250,7 +254,7 @@ def test_rollout_parity(name, kw):
 # the same schedules with the other relay schedule forced: the split one
 # (rescoring kernel, then the reroute of the flagged rows compacted per head)
 # for causal inputs, the one pass for the others
-OTHER_PATH_ROLLOUTS = [ROLLOUTS[i] for i in (0, 1, 3, 6, 7, 9, 10, 11, 12, 13, 15, 17, 18, 20)]
+OTHER_PATH_ROLLOUTS = [ROLLOUTS[i] for i in (0, 1, 3, 6, 7, 9, 10, 11, 12, 13, 15, 17, 18, 20, 22)]
 
 
 @pytest.mark.parametrize("name,kw", OTHER_PATH_ROLLOUTS,
