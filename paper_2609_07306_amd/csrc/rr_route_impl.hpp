@@ -1363,10 +1363,16 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
                 const bool exact_bm = ni <= 32 * kBmWords;
                 uint32_t *bmr = bw + r * C::SS;
                 const int32_t *lr = stg + r * STG, *ln = lr + a.k;
+                // the row's earlier draws, for the exact test past 2048
+                // chunks: in the staging slots after R and N where they fit
+                // (read back from the ledger row otherwise)
+                int32_t *ldr = stg + r * STG + a.k + a.m;
+                const bool draws_in_lds = a.r <= STG - 1 - (a.k + a.m);
 
                 // random sentinels: r draws from the valid chunks outside R u N
                 const int pool = ni - (nR + nN);
                 int32_t *out = a.led_sent + row * c_sent + a.m;
+                const int32_t *drawn = draws_in_lds ? ldr : out;
                 // exact membership of x in R u N u {first s draws}: binary
                 // searches of the id-sorted staged R and N, then the draws
                 auto in_ledger = [&](int x, int s) {
@@ -1384,7 +1390,7 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
                     }
                     if (lo < nN && ln[lo] == x) return true;
                     for (int q = 0; q < s; ++q)
-                        if (out[q] == x) return true;
+                        if (drawn[q] == x) return true;
                     return false;
                 };
                 auto marked = [&](int x, int s) {
@@ -1423,6 +1429,7 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
                         const int chosen = nth_free((int)(sm64(hs) % (uint64_t)(pool - s)), s);
                         if (chosen >= 0) atomicOr(&bmr[(chosen >> 5) & (kBmWords - 1)], 1u << (chosen & 31));
                         out[s] = chosen;
+                        if (draws_in_lds) ldr[s] = chosen;
                     }
                 } else {
                     // x mod ni by Barrett reduction: hi64(x * M) with
@@ -1467,6 +1474,7 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
                         }
                         if (chosen >= 0) atomicOr(&bmr[(chosen >> 5) & (kBmWords - 1)], 1u << (chosen & 31));
                         out[s] = chosen;
+                        if (draws_in_lds) ldr[s] = chosen;
                     }
                 }
             }
