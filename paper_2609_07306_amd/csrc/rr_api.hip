@@ -85,6 +85,11 @@ int64_t full_pairs(const rr_config &c)
     return per_head * c.n_heads;
 }
 
+// Ledger bitmap row stride of the one-pass relay in (R, C) word pairs: two
+// per 64 keys of the padded key range, plus one so that rows lie an odd
+// number of pairs apart.
+int relay_bm_words(int n_k) { return 2 * ((n_k + 63) / 64) + 1; }
+
 rr_status validate(const rr_config *c, bool ledger)
 {
     if (!c) return fail(RR_ERR_INVALID, "config is NULL");
@@ -110,6 +115,9 @@ rr_status validate(const rr_config *c, bool ledger)
     if (c->n_heads > 1024) return fail(RR_ERR_UNSUPPORTED, "n_heads must be <= 1024");
     if (rows_of(*c) * (int64_t)(c->k + m + r + 1) >= (int64_t)INT32_MAX || rows_of(*c) * c->d >= (int64_t)INT32_MAX * 8)
         return fail(RR_ERR_UNSUPPORTED, "problem too large for 32-bit row indexing");
+    if (ledger && (c->options & RR_OPT_ONE_PASS_RELAY) &&
+        relay_bm_words(c->n_k) > rr::route_relay_max_bm_words(c->dtype, c->d, c->k + c->m))
+        return fail(RR_ERR_UNSUPPORTED, "one-pass relay: the ledger bitmaps of a tile exceed its LDS (n_k too large)");
     return RR_OK;
 }
 
@@ -274,13 +282,8 @@ rr_status rr_ledger_create(const rr_config *cfg, rr_ledger **out)
     // over the padded key range, odd row stride) fit its LDS, by default for
     // causal inputs only; otherwise threshold seeds where the rescoring
     // kernel's dense tiles compute them
-    L->bm_words = 2 * ((cfg->n_k + 63) / 64) + 1;
+    L->bm_words = relay_bm_words(cfg->n_k);
     const bool fits = L->bm_words <= rr::route_relay_max_bm_words(cfg->dtype, cfg->d, cfg->k + cfg->m);
-    if ((cfg->options & RR_OPT_ONE_PASS_RELAY) && !fits) {
-        free_all(L);
-        delete L;
-        return fail(RR_ERR_UNSUPPORTED, "one-pass relay: the ledger bitmaps of a tile exceed its LDS (n_k too large)");
-    }
     L->fused = fits && ((cfg->options & RR_OPT_ONE_PASS_RELAY) ||
                         (!(cfg->options & RR_OPT_SPLIT_RELAY) && cfg->causal));
     rr::RescoreGeometry geo;

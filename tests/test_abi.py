@@ -90,6 +90,18 @@ def test_invalid_options_rejected(options):
     assert not h.value
 
 
+def test_one_pass_relay_beyond_lds_rejected():
+    """RR_OPT_ONE_PASS_RELAY where a tile's ledger bitmaps exceed its LDS
+    (n_k = 8192) is refused before anything is allocated."""
+    rr = _rr()
+    h = ctypes.c_void_p()
+    c = _cfg(n_q=8192, n_k=8192, d=128, k=32, m=16, r=16).c()
+    c.options = rr.RR_OPT_ONE_PASS_RELAY
+    assert rr.lib.rr_ledger_create(ctypes.byref(c), ctypes.byref(h)) == -5
+    assert b"one-pass" in rr.lib.rr_last_error()
+    assert not h.value
+
+
 def test_kernel_kinds_match_binding():
     """The binding sizes its profile arrays from the header's kernel kinds."""
     rr = _rr()
