@@ -126,8 +126,11 @@ rr_status rr_anchor_route(rr_ledger *ledger, int32_t layer, const void *Qc, cons
  * beta = max over C.  A row with a non-empty C and beta + gamma >= alpha is
  * rerouted: its full score row is computed and its ledger entry rebuilt as at
  * an anchor (build layer = layer, age 0).  Other rows keep their entry and get
- * age = layer - build layer.  The rerouted rows are compacted per head and
- * only they run the GEMM + TopK; with none, that step does no work.
+ * age = layer - build layer.  Only the rerouted rows run the selection and
+ * the ledger rebuild: compacted per head for a second launch (split
+ * schedule), or within the rescoring launch's own tiles (one-pass schedule);
+ * rr_config.options and the inputs choose the schedule, the results are the
+ * same.
  *   routes      optional device output [H_q*n_q, k] int32 (copy of the
  *               ledger's routes after the update); NULL to read the ledger
  *               through rr_ledger_routes instead.
