@@ -279,15 +279,15 @@ rr_status rr_ledger_create(const rr_config *cfg, rr_ledger **out)
         return st;
     }
     // relay layers in one pass where a tile's ledger bitmaps (R and C words
-    // over the padded key range, odd row stride) fit its LDS, by default for
-    // causal inputs only; otherwise threshold seeds where the rescoring
-    // kernel's dense tiles compute them
+    // over the padded key range, odd row stride) fit its LDS -- by default
+    // unless the inputs are non-causal and the rescoring would use dense
+    // tiles, whose threshold seeds make the split schedule faster there
     L->bm_words = relay_bm_words(cfg->n_k);
     const bool fits = L->bm_words <= rr::route_relay_max_bm_words(cfg->dtype, cfg->d, cfg->k + cfg->m);
-    L->fused = fits && ((cfg->options & RR_OPT_ONE_PASS_RELAY) ||
-                        (!(cfg->options & RR_OPT_SPLIT_RELAY) && cfg->causal));
     rr::RescoreGeometry geo;
     rr::rescore_geometry(rows, cfg->n_q, cfg->n_k, geo);
+    L->fused = fits && ((cfg->options & RR_OPT_ONE_PASS_RELAY) ||
+                        (!(cfg->options & RR_OPT_SPLIT_RELAY) && (cfg->causal || !geo.dense)));
     if ((L->fused && (st = alloc(&L->done, 1, "relay counter")) != RR_OK) ||
         (!L->fused && geo.dense && rr::rescore_dense_seeds(cfg->dtype, cfg->d) &&
          ((st = alloc(&L->seed_bound, rows, "seed bounds")) != RR_OK ||

@@ -251,18 +251,18 @@ def test_rollout_parity(name, kw):
     assert st["compared"] >= 0.8 * st["rows"]
 
 
-# the same schedules with the other relay schedule forced: the split one
+# the same schedules with each relay schedule forced: the split one
 # (rescoring kernel, then the reroute of the flagged rows compacted per head)
-# for causal inputs, the one pass for the others
-OTHER_PATH_ROLLOUTS = [ROLLOUTS[i] for i in (0, 1, 3, 6, 7, 9, 10, 11, 12, 13, 15, 17, 18, 20, 22)]
+# and the one pass
+FORCED_PATH_ROLLOUTS = [ROLLOUTS[i] for i in (0, 1, 3, 6, 7, 9, 10, 11, 12, 13, 15, 17, 18, 20, 21, 22)]
 
 
-@pytest.mark.parametrize("name,kw", OTHER_PATH_ROLLOUTS,
-                         ids=[f"{n}-{i}" for i, (n, _) in enumerate(OTHER_PATH_ROLLOUTS)])
-def test_rollout_parity_other_relay_path(name, kw):
+@pytest.mark.parametrize("relay", ["split", "one_pass"])
+@pytest.mark.parametrize("name,kw", FORCED_PATH_ROLLOUTS,
+                         ids=[f"{n}-{i}" for i, (n, _) in enumerate(FORCED_PATH_ROLLOUTS)])
+def test_rollout_parity_forced_relay_path(name, kw, relay):
     from parity_util import rollout_compare
     w = synth.preset(name, **kw)
-    relay = "split" if w.causal else "one_pass"
     note(f"rollout parity ({relay} relay): {name} {kw}")
     st = rollout_compare(w, relay=relay)
     note(f"  {st}")
