@@ -93,7 +93,7 @@ def _load():
         lib.orc_route_bounds.argtypes = [P, vp, vp, vp, i64, vp]
         lib.orc_anchor.argtypes = [P, i32, vp, vp, vp, i64, vp, vp, vp, vp, vp, vp]
         lib.orc_relay.argtypes = [P, i32, vp, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp,
-                                  vp]
+                                  vp, vp]
         for f in ("orc_random_sentinels", "orc_full_route", "orc_route_bounds", "orc_anchor",
                   "orc_relay"):
             getattr(lib, f).restype = ctypes.c_int
@@ -211,11 +211,14 @@ def anchor(p: Problem, layer: int, Q, K, ledger, rows=None):
 def relay(p: Problem, layer: int, Q, K, ledger, rows=None):
     """Relay layer: rescore, trigger and refresh.  Updates ``ledger`` in place.
 
-    Returns a dict with ``mask`` [rows] uint8, ``pairs``, and per-row
-    ``alpha``/``beta`` (binary64) plus ``alpha_abs``/``beta_abs``.
+    Returns a dict with ``mask`` [rows] uint8, ``pairs``, per-row
+    ``row_pairs`` (int64: |A_i| plus n_i when rerouted; -1 on rows not
+    relayed), and per-row ``alpha``/``beta`` (binary64) plus
+    ``alpha_abs``/``beta_abs``.
     """
     Q, K = _check_inputs(p, Q, K)
     rows, n = _rows_arg(rows)
+    row_pairs = np.full(p.rows, -1, dtype=np.int64)
     mask = np.zeros(p.rows, dtype=np.uint8)
     a = np.full(p.rows, np.nan)
     b = np.full(p.rows, np.nan)
@@ -225,9 +228,9 @@ def relay(p: Problem, layer: int, Q, K, ledger, rows=None):
     _rc(_load().orc_relay(ctypes.byref(p._c()), layer, _ptr(Q), _ptr(K), _ptr(rows), n,
                           _ptr(ledger["routes"]), _ptr(ledger["sent"]), _ptr(ledger["build"]),
                           _ptr(ledger["age"]), _ptr(mask), _ptr(a), _ptr(b), _ptr(aa), _ptr(ba),
-                          _ptr(pairs)))
-    return {"mask": mask, "pairs": int(pairs[0]), "alpha": a, "beta": b, "alpha_abs": aa,
-            "beta_abs": ba}
+                          _ptr(pairs), _ptr(row_pairs)))
+    return {"mask": mask, "pairs": int(pairs[0]), "row_pairs": row_pairs, "alpha": a, "beta": b,
+            "alpha_abs": aa, "beta_abs": ba}
 
 
 def recall(routes, exact) -> float:

@@ -377,11 +377,12 @@ int orc_anchor(const orc_problem *P, int32_t layer, const float *Q, const float 
 /* Intermediate layer (Sec. 3.2): each row rescores A = R u C at this layer,
  * keeps its route iff alpha > beta + gamma, otherwise refreshes.  alpha and
  * beta (and sum_t |q_t k_t| of the chunk attaining each) are returned per
- * row; beta is -inf when C has no valid slot. */
+ * row; beta is -inf when C has no valid slot.  row_pairs (if given) receives
+ * each row's own score pairs (|A| plus n_i when rerouted); pairs their sum. */
 int orc_relay(const orc_problem *P, int32_t layer, const float *Q, const float *K,
               const int64_t *rows, int64_t n_rows, int32_t *routes, int32_t *sent,
               int32_t *build, int32_t *age, uint8_t *mask, double *alpha, double *beta,
-              double *alpha_abs, double *beta_abs, int64_t *pairs)
+              double *alpha_abs, double *beta_abs, int64_t *pairs, int64_t *row_pairs)
 {
     orc_scored *work = (orc_scored *)malloc(sizeof(orc_scored) * (size_t)P->n_k);
     unsigned char *excl = (unsigned char *)malloc((size_t)P->n_k);
@@ -410,7 +411,7 @@ int orc_relay(const orc_problem *P, int32_t layer, const float *Q, const float *
             ++n_sent;
             if (s > b) { b = s; b_abs = absdot64(q, kr, P->d); }
         }
-        total += n_cand;
+        int64_t own = n_cand;
         int reroute = (n_sent > 0) && (b + P->gamma >= a);
         if (alpha) alpha[row] = a;
         if (beta) beta[row] = b;
@@ -419,10 +420,12 @@ int orc_relay(const orc_problem *P, int32_t layer, const float *Q, const float *
         if (reroute) {
             int ni;
             rebuild_row(P, layer, Q, K, row, work, excl, routes, sent, build, age, &ni);
-            total += ni;
+            own += ni;
         } else {
             age[row] = layer - build[row];
         }
+        total += own;
+        if (row_pairs) row_pairs[row] = own;
         if (mask) mask[row] = (uint8_t)reroute;
     }
     if (pairs) *pairs = total;

@@ -295,3 +295,51 @@ def test_ledger_entries_valid(causal):
         else:
             oracle.relay(p, layer, Qf, Kf, led)
         _ledger_valid(p, led)
+
+
+def test_recall_hand_computed():
+    """Recall as the Table 2 caption defines it (chunk ids of the route that
+    belong to the exact per-layer top-k, over all of the exact top-k ids),
+    on cases worked by hand: partial overlap, -1 padding on either side,
+    causal rows with fewer than k valid chunks, and order within a route."""
+    # row 0: exact {1,2,3,4}, route {1,2,5,6}: 2 hits of 4; row 1: a row with
+    # two valid chunks, exact {0,7}, route {0,7}: 2 of 2  -> 4 / 6
+    exact = np.array([[1, 2, 3, 4], [0, 7, -1, -1]])
+    got = np.array([[1, 2, 5, 6], [0, 7, -1, -1]])
+    assert oracle.recall(got, exact) == pytest.approx(4 / 6)
+    # a route is a set: its order does not matter
+    assert oracle.recall(got[:, ::-1], exact) == pytest.approx(4 / 6)
+    # -1 padding in the route is never a hit, not even against -1 padding
+    assert oracle.recall(np.full((2, 4), -1), exact) == 0.0
+    # causal early rows (n_i = 1, 2, 3 with k = 3): hits 1 + 1 + 2 of 1 + 2 + 3
+    exact3 = np.array([[0, -1, -1], [0, 1, -1], [0, 1, 2]])
+    got3 = np.array([[0, -1, -1], [1, -1, -1], [2, 1, 5]])
+    assert oracle.recall(got3, exact3) == pytest.approx(4 / 6)
+    # a perfect route, and a route disjoint from the exact set
+    assert oracle.recall(exact3, exact3) == 1.0
+    assert oracle.recall(np.array([[3, 4, 5]]), np.array([[0, 1, 2]])) == 0.0
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_row_pairs_accounting(causal):
+    """The per-row score pairs of a relay layer: |A_i| (valid candidate slots
+    of the ledger the layer starts from) plus n_i when the row is rerouted;
+    they sum to the layer's total; rows outside a relayed subset read -1."""
+    w = small(causal=causal, rho=0.3)
+    p = problem_of(w)
+    L = synth.layers(w)
+    led = oracle.new_ledger(p)
+    oracle.anchor(p, 0, L[0][0], L[0][1], led)
+    ni = np.array([p.n_valid(i % p.n_q) for i in range(p.rows)])
+    for layer in (1, 2, 3):
+        cand = n_cand(led)
+        out = oracle.relay(p, layer, L[layer][0], L[layer][1], led)
+        np.testing.assert_array_equal(out["row_pairs"], cand + out["mask"].astype(np.int64) * ni)
+        assert out["row_pairs"].sum() == out["pairs"]
+    rows = np.array([3, 17, p.rows - 1])
+    cand = n_cand(led)
+    out = oracle.relay(p, 4, L[3][0], L[3][1], led, rows=rows)
+    np.testing.assert_array_equal(out["row_pairs"][rows], cand[rows] + out["mask"][rows].astype(np.int64) * ni[rows])
+    others = np.setdiff1d(np.arange(p.rows), rows)
+    assert (out["row_pairs"][others] == -1).all()
+    assert out["pairs"] == out["row_pairs"][rows].sum()
