@@ -182,8 +182,11 @@ rr_status rr_ledger_relay_stats(const rr_ledger *ledger, float *alpha, float *be
  * rr_profile_stop every kernel the library launches is bracketed by HIP
  * events recorded on its own stream.  rr_profile_stop waits for those events
  * and returns, per kernel kind, the summed duration in milliseconds and the
- * number of launches (arrays of RR_KERNEL_KINDS entries, each may be NULL).
- * Process-wide; not for concurrent use from several threads. */
+ * number of launches.  total_ms and launches are caller arrays of n_kinds
+ * entries (each may be NULL); RR_KERNEL_KINDS entries are written, and
+ * n_kinds < RR_KERNEL_KINDS with a non-NULL array returns RR_ERR_INVALID
+ * without writing anything (profiling then stays on).  Process-wide; not for
+ * concurrent use from several threads. */
 typedef enum {
     RR_KERNEL_FULL = 0,     /* GEMM + TopK, full routing */
     RR_KERNEL_ANCHOR = 1,   /* GEMM + TopK + ledger build, every row */
@@ -194,7 +197,23 @@ typedef enum {
 } rr_kernel_kind;
 
 rr_status rr_profile_start(void);
-rr_status rr_profile_stop(double *total_ms, int64_t *launches);
+rr_status rr_profile_stop(double *total_ms, int64_t *launches, int32_t n_kinds);
+
+/* Exact selection (Eq. (2)) runs collection sweeps over a row's keys until
+ * the row's candidate list holds exactly its top k+m (bisection on the score,
+ * then on the chunk id of a tied score); the number of sweeps is capped above
+ * what the bisections can need.  A row that still had not settled at the cap
+ * would get an empty routed and near-miss set, and is counted here.
+ * rr_unconverged_rows synchronises the current device and stores, in *count
+ * (host memory), the number of such rows over every call on that device since
+ * the library was loaded: 0 unless something is wrong.  A diagnostic, not for
+ * the hot path. */
+rr_status rr_unconverged_rows(uint64_t *count);
+
+/* Test hook: caps the collection sweeps per route tile at `cap` for later
+ * launches from this process (0 restores the default cap; the default always
+ * suffices).  A lowered cap exists only to exercise rr_unconverged_rows. */
+rr_status rr_set_sweep_cap(int32_t cap);
 
 /* Number of bytes of ledger index storage (routes plus sentinels) for a
  * config: H_q * n_q * (k + m + r) * 4. */

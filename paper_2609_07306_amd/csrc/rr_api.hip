@@ -3,8 +3,10 @@
 // route (GEMM + TopK) and rescoring kernels.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -30,9 +32,29 @@ struct rr_ledger {
     int64_t *stat_pairs;
 };
 
+// Device-resident library state, one copy per GPU: the running count of rows
+// whose selection stopped at the collection-sweep cap.
+static __device__ unsigned long long g_unconverged_dev;
+
 namespace {
 
 thread_local std::string g_err;
+
+constexpr int kMaxDevices = 64;
+
+// Per-device addresses of the device-resident state, resolved with
+// hipGetSymbolAddress once per device (with that device current): in host
+// code the variable's name is a host-side stand-in, not a device address.
+struct DeviceState {
+    std::atomic<bool> ready{false};
+    unsigned long long *unconverged = nullptr;
+};
+DeviceState g_devstate[kMaxDevices];
+std::mutex g_devstate_mu;
+
+// Collection sweeps allowed per route tile (0: the kernel's default cap);
+// lowered only by the test hook rr_set_sweep_cap.
+std::atomic<int> g_sweep_cap{0};
 
 // Diagnostics: the flagged rows of each head as an ascending id list
 // (ballot + prefix over the head's flags), -1 after the last.  One
@@ -202,10 +224,34 @@ hipError_t timed(int kind, hipStream_t stream, F fn)
     return e;
 }
 
+// The current device's state (resolving its addresses on first use), or an
+// error status with the message set.
+rr_status device_state(DeviceState **out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(RR_ERR_UNSUPPORTED, "device ordinal beyond the library's table");
+    DeviceState &st = g_devstate[dev];
+    if (!st.ready.load(std::memory_order_acquire)) {
+        std::lock_guard<std::mutex> lock(g_devstate_mu);
+        if (!st.ready.load(std::memory_order_relaxed)) {
+            void *p = nullptr;
+            e = hipGetSymbolAddress(&p, HIP_SYMBOL(g_unconverged_dev));
+            if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress (unconverged-row counter)");
+            st.unconverged = static_cast<unsigned long long *>(p);
+            st.ready.store(true, std::memory_order_release);
+        }
+    }
+    *out = &st;
+    return RR_OK;
+}
+
 rr::RouteArgs route_args(const rr_config &c, const void *Q, const void *K)
 {
     rr::RouteArgs a;
     std::memset(&a, 0, sizeof(a));
+    a.sweep_cap = g_sweep_cap.load(std::memory_order_relaxed);
     a.Q = Q;
     a.K = K;
     a.n_heads = c.n_heads;
@@ -332,8 +378,12 @@ rr_status rr_anchor_route(rr_ledger *L, int32_t layer, const void *Qc, const voi
     if (!Qc || !Kc) return fail(RR_ERR_INVALID, "Qc and Kc must be device pointers");
     if (layer < 0) return fail(RR_ERR_INVALID, "layer must be >= 0");
     DeviceGuard g(L->device);
+    DeviceState *ds = nullptr;
+    rr_status st = device_state(&ds);
+    if (st != RR_OK) return st;
     const rr_config &c = L->cfg;
     rr::RouteArgs a = route_args(c, Qc, Kc);
+    a.unconverged = ds->unconverged;
     a.layer = layer;
     a.mode = rr::MODE_ANCHOR;
     a.routes_out = routes;
@@ -360,6 +410,9 @@ rr_status rr_relay_layer(rr_ledger *L, int32_t layer, const void *Qc, const void
     if (!L->has_state) return fail(RR_ERR_STATE, "relay before any anchor or import");
     if (layer < L->last_layer) return fail(RR_ERR_STATE, "layer is below the previous call's layer");
     DeviceGuard g(L->device);
+    DeviceState *ds = nullptr;
+    rr_status st = device_state(&ds);
+    if (st != RR_OK) return st;
     const rr_config &c = L->cfg;
     hipStream_t stream = reinterpret_cast<hipStream_t>(hip_stream);
 
@@ -367,6 +420,7 @@ rr_status rr_relay_layer(rr_ledger *L, int32_t layer, const void *Qc, const void
         // one pass: each tile rescores its rows' ledgers on its own scores,
         // flags them, and routes the flagged rows into the ledger
         rr::RouteArgs a = route_args(c, Qc, Kc);
+        a.unconverged = ds->unconverged;
         a.layer = layer;
         a.mode = rr::MODE_RELAY;
         a.led_routes = L->routes;
@@ -428,6 +482,7 @@ rr_status rr_relay_layer(rr_ledger *L, int32_t layer, const void *Qc, const void
         if (e != hipSuccess) return hip_fail(e, "rescore launch");
 
         rr::RouteArgs a = route_args(c, Qc, Kc);
+        a.unconverged = ds->unconverged;
         a.layer = layer;
         a.mode = rr::MODE_REROUTE;
         a.led_routes = L->routes;
@@ -464,10 +519,13 @@ rr_status rr_full_route(const rr_config *cfg, const void *Qc, const void *Kc, in
     rr_status st = validate(cfg, false);
     if (st != RR_OK) return st;
     if (!Qc || !Kc || !routes) return fail(RR_ERR_INVALID, "Qc, Kc and routes must be device pointers");
+    DeviceState *ds = nullptr;
+    if ((st = device_state(&ds)) != RR_OK) return st;
     rr_config c = *cfg;
     c.m = 0;
     c.r = 0;
     rr::RouteArgs a = route_args(c, Qc, Kc);
+    a.unconverged = ds->unconverged;
     a.mode = rr::MODE_FULL;
     a.routes_out = routes;
     a.scores_out = route_scores;
@@ -545,8 +603,10 @@ rr_status rr_profile_start(void)
     return RR_OK;
 }
 
-rr_status rr_profile_stop(double *total_ms, int64_t *launches)
+rr_status rr_profile_stop(double *total_ms, int64_t *launches, int32_t n_kinds)
 {
+    if ((total_ms || launches) && n_kinds < RR_KERNEL_KINDS)
+        return fail(RR_ERR_INVALID, "rr_profile_stop: the arrays must hold RR_KERNEL_KINDS entries");
     g_prof.on = false;
     double ms[RR_KERNEL_KINDS] = {};
     int64_t n[RR_KERNEL_KINDS] = {};
@@ -567,6 +627,24 @@ rr_status rr_profile_stop(double *total_ms, int64_t *launches)
         if (launches) launches[k] = n[k];
     }
     return st;
+}
+
+rr_status rr_unconverged_rows(uint64_t *count)
+{
+    if (!count) return fail(RR_ERR_INVALID, "count is NULL");
+    DeviceState *ds = nullptr;
+    rr_status st = device_state(&ds);
+    if (st != RR_OK) return st;
+    hipError_t e = hipDeviceSynchronize();
+    if (e == hipSuccess) e = hipMemcpy(count, ds->unconverged, sizeof(uint64_t), hipMemcpyDeviceToHost);
+    return e == hipSuccess ? RR_OK : hip_fail(e, "unconverged-row count");
+}
+
+rr_status rr_set_sweep_cap(int32_t cap)
+{
+    if (cap < 0) return fail(RR_ERR_INVALID, "the sweep cap must be >= 0 (0: the default)");
+    g_sweep_cap.store(cap, std::memory_order_relaxed);
+    return RR_OK;
 }
 
 }  // extern "C"

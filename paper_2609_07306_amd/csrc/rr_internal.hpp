@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 namespace rr {
 
 enum RouteMode : int32_t {
@@ -56,7 +58,33 @@ struct RouteArgs {
     uint32_t *done;            // relay: finished-workgroup counter (0 between launches)
     int64_t *pairs_out;        // optional device scalar
     int64_t pairs_value;       // value written to pairs_out (full / anchor; reroute: the workgroup sums)
+    unsigned long long *unconverged;  // device counter: rows whose collection stopped at the sweep cap
+    int32_t sweep_cap;                // collection sweeps allowed per tile (kMaxFixIters unless a test lowers it)
 };
+
+// Raises a kernel's dynamic LDS limit on the current device when a launch
+// needs more than any earlier one there (the default limit is 64 KiB), so
+// the runtime call is made once per kernel instance and device rather than
+// on every launch.  `seen` is the instance's own record, zero-initialised.
+struct LdsLimit {
+    std::atomic<int> bytes[64];
+};
+
+inline hipError_t raise_lds_limit(const void *fn, size_t lds, LdsLimit &seen)
+{
+    if (lds <= 65536) return hipSuccess;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev >= 0 && dev < 64 && seen.bytes[dev].load(std::memory_order_acquire) >= (int)lds) return hipSuccess;
+    e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e == hipSuccess && dev >= 0 && dev < 64) {
+        int cur = seen.bytes[dev].load(std::memory_order_relaxed);
+        while (cur < (int)lds && !seen.bytes[dev].compare_exchange_weak(cur, (int)lds)) {
+        }
+    }
+    return e;
+}
 
 
 // Supported (dtype, d) combinations; dtype 0 = binary32, 1 = bf16.

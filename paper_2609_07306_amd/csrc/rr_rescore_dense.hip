@@ -289,10 +289,9 @@ hipError_t launch_n(const RescoreArgs &a, hipStream_t stream)
     size_t lds = (size_t)2 * C::ST + (size_t)C::BM * a.bm_words * sizeof(uint2);
     if (kDenseSeeds<DT, D>) lds = std::max(lds, (size_t)C::BM * C::UST * sizeof(float));  // the kept scores
     const void *fn = reinterpret_cast<const void *>(&rescore_dense_kernel<DT, D, NW>);
-    if (lds > 65536) {
-        const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
-    }
+    static LdsLimit seen;
+    const hipError_t e = raise_lds_limit(fn, lds, seen);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL((rescore_dense_kernel<DT, D, NW>), dim3(a.n_heads * a.blocks_per_head), dim3(C::NT), lds,
                        stream, a);
     return hipGetLastError();

@@ -24,7 +24,7 @@ EXPORTED = (
     "rr_ledger_create", "rr_ledger_destroy", "rr_anchor_route", "rr_relay_layer", "rr_full_route",
     "rr_ledger_routes", "rr_ledger_export", "rr_ledger_import", "rr_ledger_relay_stats",
     "rr_ledger_index_bytes", "rr_status_string", "rr_last_error", "rr_profile_start",
-    "rr_profile_stop",
+    "rr_profile_stop", "rr_unconverged_rows", "rr_set_sweep_cap",
 )
 KERNEL_KINDS = ("full", "anchor", "reroute", "rescore", "relay")
 
@@ -63,7 +63,9 @@ def _load():
         "rr_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "rr_last_error": (ctypes.c_char_p, []),
         "rr_profile_start": (ctypes.c_int, []),
-        "rr_profile_stop": (ctypes.c_int, [vp, vp]),
+        "rr_profile_stop": (ctypes.c_int, [vp, vp, i32]),
+        "rr_unconverged_rows": (ctypes.c_int, [ctypes.POINTER(ctypes.c_uint64)]),
+        "rr_set_sweep_cap": (ctypes.c_int, [i32]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -158,8 +160,20 @@ def profile_stop():
     """Stop profiling; returns {kind: (total_ms, launches)}."""
     ms = (ctypes.c_double * len(KERNEL_KINDS))()
     n = (ctypes.c_int64 * len(KERNEL_KINDS))()
-    _check(lib.rr_profile_stop(ms, n))
+    _check(lib.rr_profile_stop(ms, n, len(KERNEL_KINDS)))
     return {k: (ms[i], n[i]) for i, k in enumerate(KERNEL_KINDS)}
+
+
+def unconverged_rows() -> int:
+    """Rows (on the current device, since load) whose selection stopped at the sweep cap."""
+    c = ctypes.c_uint64()
+    _check(lib.rr_unconverged_rows(ctypes.byref(c)))
+    return int(c.value)
+
+
+def set_sweep_cap(cap: int):
+    """Test hook: collection sweeps allowed per route tile (0: default)."""
+    _check(lib.rr_set_sweep_cap(int(cap)))
 
 
 def index_bytes(cfg: Config) -> int:

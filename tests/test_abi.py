@@ -129,3 +129,32 @@ def test_ledger_index_bytes_paper_figure():
     rr = _rr()
     cfg = rr.Config(1, 1, 1024, 1024, 128, 32, 16, 16)
     assert rr.index_bytes(cfg) == 256 * 1024
+
+
+def test_profile_stop_rejects_short_arrays():
+    """rr_profile_stop takes the length of its output arrays: a length below
+    RR_KERNEL_KINDS is refused before anything is written (an earlier
+    signature without the length let a binding sized for fewer kinds overrun
+    its arrays)."""
+    rr = _rr()
+    n = len(rr.KERNEL_KINDS)
+    ms = (ctypes.c_double * (n + 2))(*([-7.0] * (n + 2)))
+    cnt = (ctypes.c_int64 * (n + 2))(*([-7] * (n + 2)))
+    assert rr.lib.rr_profile_start() == 0
+    assert rr.lib.rr_profile_stop(ms, cnt, n - 1) == -1
+    assert b"RR_KERNEL_KINDS" in rr.lib.rr_last_error()
+    assert list(ms) == [-7.0] * (n + 2) and list(cnt) == [-7] * (n + 2)
+    # the full length succeeds and writes exactly RR_KERNEL_KINDS entries
+    # (nothing was launched, so every kind reads zero)
+    assert rr.lib.rr_profile_stop(ms, cnt, n + 2) == 0
+    assert list(ms[:n]) == [0.0] * n and list(cnt[:n]) == [0] * n
+    assert list(ms[n:]) == [-7.0, -7.0] and list(cnt[n:]) == [-7, -7]
+    # NULL arrays need no length
+    assert rr.lib.rr_profile_stop(None, None, 0) == 0
+
+
+def test_sweep_cap_hook_validates():
+    rr = _rr()
+    assert rr.lib.rr_set_sweep_cap(-1) == -1
+    assert rr.lib.rr_set_sweep_cap(0) == 0
+    assert rr.lib.rr_unconverged_rows(None) == -1
