@@ -10,6 +10,13 @@ with tau = max(1e-4 * max|s|, 2 d 2^-24 * max sum_t |q_t k_t|): the relative
 band of the accepted tie rule, never narrower than the binary32 dot-product
 error bound.  A row whose outcome was excluded stays excluded (tainted) until
 the next anchor rebuilds it without a tie.
+
+Scores (alpha, beta) are checked two ways: within TOL of sum_t |q_t k_t|
+(the dot product's condition scale) on every trusted row, and within TOL of
+|s| itself -- the literal relative error -- wherever the binary32
+accumulation bound 2 d 2^-24 sum_t |q_t k_t| lies below TOL |s| (elsewhere a
+binary32 dot product cannot promise that relative error).  The largest
+literal |delta| / |s| over all trusted rows is reported.
 """
 from __future__ import annotations
 
@@ -70,6 +77,26 @@ def ledger_np(L: rr.Ledger):
     return {k: v.cpu().numpy() for k, v in e.items()}
 
 
+def score_check(got, ref, ref_abs, d, dtype, stats=None):
+    """Checks binary32 scores against the oracle's binary64 ones (finite
+    entries): within TOL * sum|qk| everywhere, within TOL * |s| where the
+    accumulation bound allows; accumulates the literal relative error."""
+    tol = TOL[dtype]
+    fin = np.isfinite(ref)
+    got, ref, ref_abs = got[fin], ref[fin], ref_abs[fin]
+    delta = np.abs(got.astype(np.float64) - ref)
+    assert np.all(delta <= tol * ref_abs + 1e-30), f"score error {delta.max()} beyond {tol} * sum|qk|"
+    lit = 2 * d * 2.0 ** -24 * ref_abs <= tol * np.abs(ref)
+    assert np.all(delta[lit] <= tol * np.abs(ref[lit])), "literal relative score error beyond tolerance"
+    if stats is not None:
+        with np.errstate(divide="ignore", invalid="ignore"):
+            rel = np.where(ref != 0, delta / np.abs(ref), 0.0)
+        if len(rel):
+            stats["rel_err_max"] = max(stats.get("rel_err_max", 0.0), float(rel.max()))
+        stats["rel_checked"] = stats.get("rel_checked", 0) + int(lit.sum())
+        stats["scores_checked"] = stats.get("scores_checked", 0) + int(fin.sum())
+
+
 def n_valid_rows(p):
     i = np.arange(p.rows) % p.n_q
     return np.minimum(i + 1, p.n_k) if p.causal else np.full(p.rows, p.n_k)
@@ -93,7 +120,7 @@ def rollout_compare(w, gamma=None, check_scores=True, relay="auto"):
     mask_t = torch.empty(p.rows, dtype=torch.uint8, device=device)
     pairs_t = torch.zeros(1, dtype=torch.int64, device=device)
     nrr_t = torch.zeros(1, dtype=torch.int32, device=device)
-    stats = {"rows": 0, "compared": 0, "ties": 0, "rerouted": 0, "relay_rows": 0}
+    stats = {"rows": 0, "compared": 0, "ties": 0, "rerouted": 0, "relay_rows": 0, "pair_rows_compared": 0}
     for layer, Qf, Kf, Qd, Kd in synth.Generator(w):
         Q, K = dev(Qd, w.dtype), dev(Kd, w.dtype)
         t1, t2 = route_ties(p, Qf, Kf)
@@ -121,10 +148,19 @@ def rollout_compare(w, gamma=None, check_scores=True, relay="auto"):
             for key in ("routes", "sent", "build", "age"):
                 a, b = got[key][new_trusted], ref[key][new_trusted]
                 assert np.array_equal(a, b), f"relay layer {layer}: {key} differs"
-            # score pairs: the GPU's own accounting, and equality with the oracle
+            # score pairs: the kernel's total is the sum of its rows'
+            # contributions (|A_i| of the ledger it started from, plus n_i when
+            # rerouted); on every decided row that contribution equals the
+            # oracle's, and the totals agree once the other rows are set aside
             cand = (before["routes"] >= 0).sum(1) + (before["sent"] >= 0).sum(1)
-            assert int(pairs_t.item()) == int(cand.sum() + ni[gmask].sum())
+            gpu_row_pairs = cand + gmask.astype(np.int64) * ni
+            assert int(pairs_t.item()) == int(gpu_row_pairs.sum())
             assert int(nrr_t.item()) == int(gmask.sum())
+            bad = np.flatnonzero(decided & (gpu_row_pairs != out["row_pairs"]))
+            assert len(bad) == 0, f"relay layer {layer}: score pairs differ on rows {bad[:8]}"
+            assert int(pairs_t.item()) - int(gpu_row_pairs[~decided].sum()) == \
+                out["pairs"] - int(out["row_pairs"][~decided].sum())
+            stats["pair_rows_compared"] += int(decided.sum())
             if np.array_equal(gmask, omask) and trusted.all():
                 assert int(pairs_t.item()) == out["pairs"]
             if check_scores:
@@ -137,17 +173,109 @@ def rollout_compare(w, gamma=None, check_scores=True, relay="auto"):
                     fl = np.flatnonzero(gmask.reshape(p.n_heads, p.n_q)[h])
                     np.testing.assert_array_equal(ids[h, :len(fl)], fl)
                     assert np.all(ids[h, len(fl):] == -1)
-                tol = TOL[w.dtype]
                 ok = trusted
-                assert np.all(np.abs(alpha[ok] - out["alpha"][ok]) <= tol * out["alpha_abs"][ok] + 1e-30)
-                fin = ok & np.isfinite(out["beta"])
-                assert np.all(np.abs(beta[fin] - out["beta"][fin]) <= tol * out["beta_abs"][fin] + 1e-30)
+                score_check(alpha[ok], out["alpha"][ok], out["alpha_abs"][ok], p.d, w.dtype, stats)
+                score_check(beta[ok], out["beta"][ok], out["beta_abs"][ok], p.d, w.dtype, stats)
                 assert np.all(np.isneginf(beta[ok & ~np.isfinite(out["beta"])]))
+                assert np.all(np.isposinf(alpha[ok & np.isposinf(out["alpha"])]))
             stats["rerouted"] += int(gmask.sum())
             stats["relay_rows"] += p.rows
             trusted = new_trusted
         stats["rows"] += p.rows
         stats["compared"] += int(trusted.sum())
         stats["ties"] += int((~trusted).sum())
+    L.close()
+    return stats
+
+
+def _oracle_threads(fn, p, head_rows):
+    """Runs fn(rows) for each head's row block in its own thread (the C
+    oracle holds no global state and ctypes releases the GIL; the heads'
+    rows are disjoint, so the ledger arrays are written without overlap)."""
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(max_workers=len(head_rows)) as ex:
+        return list(ex.map(fn, head_rows))
+
+
+def rollout_subset(w, heads, layers, relay="auto", note=print):
+    """The workload at its full size on the GPU (every head, the launch
+    configuration the benchmark times) against the oracle on the rows of the
+    listed query heads only, over ``layers`` (a range that starts at an
+    anchor layer).  Every anchor and relay layer is compared tie-aware on
+    those rows: ledger rows, mask, alpha / beta, per-row score pairs.
+    Returns the statistics dict of rollout_compare."""
+    p = problem_of(w)
+    assert w.is_anchor(layers.start), "a subset rollout starts at an anchor"
+    cfg = dataclasses.replace(rr.Config.of(w), relay=relay)
+    L = rr.Ledger(cfg)
+    ref = oracle.new_ledger(p)
+    head_rows = [np.arange(h * p.n_q, (h + 1) * p.n_q, dtype=np.int64) for h in heads]
+    rows = np.concatenate(head_rows)
+    ni = n_valid_rows(p)[rows]
+    trusted = np.zeros(len(rows), dtype=bool)
+    device = torch.device("cuda", torch.cuda.current_device())
+    mask_t = torch.empty(p.rows, dtype=torch.uint8, device=device)
+    pairs_t = torch.zeros(1, dtype=torch.int64, device=device)
+    stats = {"rows": 0, "compared": 0, "ties": 0, "rerouted": 0, "relay_rows": 0, "pair_rows_compared": 0,
+             "tie_rows_per_layer": []}
+
+    def sub(led):
+        return {k: v[rows] for k, v in led.items()}
+
+    for layer, Qf, Kf, Qd, Kd in synth.Generator(w):
+        if layer < layers.start:
+            continue
+        if layer >= layers.stop:
+            break
+        Q, K = dev(Qd, w.dtype), dev(Kd, w.dtype)
+        bounds = np.concatenate(_oracle_threads(lambda r: oracle.route_bounds(p, Qf, Kf, r), p, head_rows))
+        t1 = gap_tie(bounds[:, 0], bounds[:, 1], bounds[:, 4], bounds[:, 5], p.d)
+        t2 = gap_tie(bounds[:, 2], bounds[:, 3], bounds[:, 6], bounds[:, 7], p.d)
+        if w.is_anchor(layer):
+            L.anchor(layer, Q, K)
+            _oracle_threads(lambda r: oracle.anchor(p, layer, Qf, Kf, ref, rows=r), p, head_rows)
+            got = sub(ledger_np(L))
+            trusted = ~(t1 | t2)
+            for key in ("routes", "sent", "build", "age"):
+                a, b = got[key][trusted], ref[key][rows][trusted]
+                assert np.array_equal(a, b), f"anchor layer {layer}: {key} differs"
+            stats["tie_rows_per_layer"].append(int((t1 | t2).sum()))
+        else:
+            before = sub(ledger_np(L))
+            L.relay(layer, Q, K, mask=mask_t, pairs=pairs_t)
+            outs = _oracle_threads(lambda r: oracle.relay(p, layer, Qf, Kf, ref, rows=r), p, head_rows)
+            out = {k: np.concatenate([o[k][r] for o, r in zip(outs, head_rows)])
+                   for k in ("mask", "row_pairs", "alpha", "beta", "alpha_abs", "beta_abs")}
+            got = sub(ledger_np(L))
+            gmask = mask_t.cpu().numpy().astype(bool)[rows]
+            omask = out["mask"].astype(bool)
+            with np.errstate(invalid="ignore"):
+                t3 = (np.abs(out["alpha"] - (out["beta"] + p.gamma)) <
+                      tau(out["alpha"], out["beta"], out["alpha_abs"], out["beta_abs"], p.d))
+            decided = trusted & ~t3
+            bad = np.flatnonzero(decided & (gmask != omask))
+            assert len(bad) == 0, f"relay layer {layer}: mask differs on rows {rows[bad[:8]]}"
+            new_trusted = decided & ~(omask & (t1 | t2))
+            for key in ("routes", "sent", "build", "age"):
+                a, b = got[key][new_trusted], ref[key][rows][new_trusted]
+                assert np.array_equal(a, b), f"relay layer {layer}: {key} differs"
+            cand = (before["routes"] >= 0).sum(1) + (before["sent"] >= 0).sum(1)
+            gpu_row_pairs = cand + gmask.astype(np.int64) * ni
+            bad = np.flatnonzero(decided & (gpu_row_pairs != out["row_pairs"]))
+            assert len(bad) == 0, f"relay layer {layer}: score pairs differ on rows {rows[bad[:8]]}"
+            stats["pair_rows_compared"] += int(decided.sum())
+            alpha, beta, _ = L.relay_stats()
+            torch.cuda.synchronize()
+            alpha, beta = alpha.cpu().numpy()[rows], beta.cpu().numpy()[rows]
+            score_check(alpha[trusted], out["alpha"][trusted], out["alpha_abs"][trusted], p.d, w.dtype, stats)
+            score_check(beta[trusted], out["beta"][trusted], out["beta_abs"][trusted], p.d, w.dtype, stats)
+            stats["rerouted"] += int(gmask.sum())
+            stats["relay_rows"] += len(rows)
+            stats["tie_rows_per_layer"].append(int((~new_trusted).sum()))
+            trusted = new_trusted
+        stats["rows"] += len(rows)
+        stats["compared"] += int(trusted.sum())
+        stats["ties"] += int((~trusted).sum())
+        note(f"  layer {layer}: compared {int(trusted.sum())} of {len(rows)} rows")
     L.close()
     return stats

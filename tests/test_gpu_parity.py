@@ -374,6 +374,35 @@ def test_full_size_sampled(name, kw):
     L.close()
 
 
+# Full-size rollouts on a head subset: the GPU runs every head of the
+# workload (the benchmark's launch configuration), the oracle the rows of a
+# few heads, over all 32 layers in segments of one anchor plus seven relays
+# (the anchor at the start of each segment rebuilds every ledger entry, so
+# segments are independent).
+# The long-context workload crowds its top-k boundaries on purpose (a quarter
+# of the keys are near-duplicates), so rows whose outcome hinges on a near tie
+# accumulate until the next anchor: about a third of the rows are set aside
+# by the eighth layer of a segment, hence its lower floor of compared rows.
+SUBSET_ROLLOUTS = [
+    ("scale", {}, (0, 31), range(0, 32), 0.8),
+    ("longctx", {}, (0, 17), range(0, 8), 0.6),
+    ("longctx", {}, (0, 17), range(8, 16), 0.6),
+    ("longctx", {}, (0, 17), range(16, 24), 0.6),
+    ("longctx", {}, (0, 17), range(24, 32), 0.6),
+]
+
+
+@pytest.mark.parametrize("name,kw,heads,layers,floor", SUBSET_ROLLOUTS,
+                         ids=[f"{n}-layers{l.start}-{l.stop - 1}" for n, _, _, l, _ in SUBSET_ROLLOUTS])
+def test_full_size_head_subset_rollout(name, kw, heads, layers, floor):
+    from parity_util import rollout_subset
+    w = synth.preset(name, **kw)
+    note(f"full-size head-subset rollout: {w.name} n={w.n} heads {heads} of {w.n_heads}, layers {layers.start}..{layers.stop - 1}")
+    st = rollout_subset(w, heads, layers, note=note)
+    note(f"  {st}")
+    assert st["compared"] >= floor * st["rows"]
+
+
 def test_state_errors():
     from parity_util import dev
     rr = rrmod()
@@ -388,4 +417,44 @@ def test_state_errors():
         L.relay(2, Q, Q)
     assert e.value.status == rr.RR_ERR_STATE
     L.relay(3, Q, Q)
+    L.close()
+
+
+def test_sweep_cap_counts_unconverged_rows():
+    """The collection loop's sweep cap lies above what the bisections need:
+    with the default cap no row is counted.  With the cap lowered to one sweep
+    (a test hook) on inputs whose massive exact ties need repair sweeps, the
+    rows left unsettled are counted by rr_unconverged_rows, and their ledger
+    entries hold valid ids only (empty R and N, sentinels from the valid
+    chunks)."""
+    from parity_util import dev, ledger_np
+    rr = rrmod()
+    rng = np.random.default_rng(5)
+    H, n, d, k, m, r = 2, 300, 32, 24, 12, 8
+    Q = rng.integers(-2, 3, size=(H, n, d)).astype(np.float32)
+    K = rng.integers(-1, 2, size=(H, n, d)).astype(np.float32)
+    cfg = rr.Config(H, H, n, n, d, k, m, r, "f32", False)
+    note("sweep cap: default, then one sweep")
+    before = rr.unconverged_rows()
+    L = rr.Ledger(cfg)
+    L.anchor(0, dev(Q, "f32"), dev(K, "f32"))
+    ref = oracle.new_ledger(oracle.Problem(H, H, n, n, d, k, m, r))
+    oracle.anchor(oracle.Problem(H, H, n, n, d, k, m, r), 0, Q, K, ref)
+    got = ledger_np(L)
+    np.testing.assert_array_equal(got["routes"], ref["routes"])
+    assert rr.unconverged_rows() == before
+    try:
+        rr.set_sweep_cap(1)
+        L.anchor(1, dev(Q, "f32"), dev(K, "f32"))
+        torch.cuda.synchronize()
+    finally:
+        rr.set_sweep_cap(0)
+    counted = rr.unconverged_rows() - before
+    got = ledger_np(L)
+    empty = (got["routes"] == -1).all(1)
+    note(f"  unconverged rows at one sweep: {counted}")
+    assert counted > 0 and counted == int(empty.sum())
+    assert ((got["sent"] >= -1) & (got["sent"] < n)).all()
+    # rows that settled in one sweep are exact
+    np.testing.assert_array_equal(got["routes"][~empty], ref["routes"][~empty])
     L.close()
