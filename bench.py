@@ -13,10 +13,15 @@ are resident in HBM before timing.  The baseline step runs full routing
 (the same GEMM + TopK kernel) at every layer.
 
 Output: one JSON line.  ``value`` = routed rows per second per layer of the
-RouteRelay schedule (H * n_q * L / step time).  ``roofline`` describes the
-kernel with the largest share of the step, timed with HIP events the library
-records on its launch stream; ``cpu_baseline`` times the oracle on a head
-subset of the same workload on this host.
+RouteRelay schedule (H * n_q * L / step time over the K timed steps); the
+median step and its p10 / p90 are reported beside it (the paper times
+medians).  ``roofline`` describes the kernel with the largest share of the
+step, timed with HIP events the library records on its launch stream;
+``cpu_baseline`` times the oracle on a head subset of the same workload on
+this host's cores (``cpu_baseline_1thread``: one thread).  Also reported:
+per-layer near-tie counts, fidelity (recall, rerouted fraction, score pairs)
+averaged over seeds 0, 1, 2, the low-drift operating points of the same
+shape, and measured copy and GEMM rates beside the nominal peaks.
 """
 from __future__ import annotations
 
@@ -76,7 +81,34 @@ def parse():
     ap.add_argument("--no-full", action="store_true", help="skip the full-routing baseline")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a device-to-device copy of MIB MiB (calibrates the HBM byte counters)")
+    ap.add_argument("--low-drift", default="0.005,0.01,0.02",
+                    help="extra operating points: comma-separated rho values of the same shape ('' for none)")
+    ap.add_argument("--seeds", default="1,2", help="extra seeds for the fidelity average ('' for none)")
+    ap.add_argument("--cpu-threads", type=int, default=0, help="oracle threads for cpu_baseline (0: the host's cores, at most 16)")
     return ap.parse_args()
+
+
+def pct(x, q):
+    import numpy as np
+    return float(np.percentile(np.asarray(x, dtype=np.float64), q))
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def host_cores() -> int:
+    try:
+        return len(os.sched_getaffinity(0))
+    except AttributeError:
+        return os.cpu_count() or 1
 
 
 def describe(w) -> str:
@@ -89,6 +121,215 @@ def describe(w) -> str:
     if w.near_ties:
         parts.append("25% near-tie duplicate keys")
     return ", ".join(parts)
+
+
+def upload(w, dev, keep_cpu_heads=0):
+    """All layers of a workload on the device (and, if asked, the binary32
+    values of the first keep_cpu_heads query heads and their key heads)."""
+    from paper_2609_07306_amd import routerelay as rr
+    from paper_2609_07306_amd import synth
+    import numpy as np
+    group = w.n_heads // w.n_kv_heads
+    Qd, Kd, cpu = [], [], []
+    for layer, Qf, Kf, Qx, Kx in synth.Generator(w):
+        Qd.append(rr.to_device(Qx, w.dtype, dev))
+        Kd.append(rr.to_device(Kx, w.dtype, dev))
+        if keep_cpu_heads:
+            cpu.append((np.ascontiguousarray(Qf[:keep_cpu_heads]),
+                        np.ascontiguousarray(Kf[: keep_cpu_heads // group])))
+    return Qd, Kd, cpu
+
+
+class Schedule:
+    """The RouteRelay schedule of a workload on one ledger, its full-routing
+    baseline, and the fidelity of one pass."""
+
+    def __init__(self, w, cfg, Qd, Kd, dev):
+        import torch
+        from paper_2609_07306_amd import routerelay as rr
+        self.w, self.cfg, self.Qd, self.Kd, self.rr = w, cfg, Qd, Kd, rr
+        L, rows = w.n_layers, cfg.rows
+        self.led = rr.Ledger(cfg)
+        self.masks = torch.zeros((L, rows), dtype=torch.uint8, device=dev)
+        self.pairs = torch.zeros((L, 1), dtype=torch.int64, device=dev)
+        self.nrr = torch.zeros((L, 1), dtype=torch.int32, device=dev)
+        self.full_routes = torch.empty((L, rows, w.k), dtype=torch.int32, device=dev)
+        self.relay_routes = torch.empty((L, rows, w.k), dtype=torch.int32, device=dev)
+
+    def relay_step(self, keep_routes=False, marks=None):
+        w, led = self.w, self.led
+        for l in range(w.n_layers):
+            if marks is not None:
+                marks[l].record()
+            out = self.relay_routes[l] if keep_routes else None
+            if w.is_anchor(l):
+                led.anchor(l, self.Qd[l], self.Kd[l], routes=out, pairs=self.pairs[l])
+            else:
+                led.relay(l, self.Qd[l], self.Kd[l], routes=out, mask=self.masks[l], pairs=self.pairs[l],
+                          n_rerouted=self.nrr[l])
+        if marks is not None:
+            marks[w.n_layers].record()
+
+    def full_step(self):
+        for l in range(self.w.n_layers):
+            self.rr.full_route(self.cfg, self.Qd[l], self.Kd[l], self.full_routes[l])
+
+    def timed(self, fn, steps):
+        """K steps bracketed by synchronisation: (mean ms per step, per-step ms)."""
+        import torch
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        torch.cuda.synchronize()
+        ev[0].record()
+        for t in range(steps):
+            fn()
+            ev[t + 1].record()
+        torch.cuda.synchronize()
+        per = [ev[t].elapsed_time(ev[t + 1]) for t in range(steps)]
+        return ev[0].elapsed_time(ev[steps]) / steps, per
+
+    def layer_times(self, steps):
+        """Per-layer durations (ms), [steps, L], from events between library calls."""
+        import numpy as np
+        import torch
+        L = self.w.n_layers
+        out = np.zeros((steps, L))
+        for t in range(steps):
+            marks = [torch.cuda.Event(enable_timing=True) for _ in range(L + 1)]
+            self.relay_step(marks=marks)
+            torch.cuda.synchronize()
+            out[t] = [marks[l].elapsed_time(marks[l + 1]) for l in range(L)]
+        return out
+
+    def fidelity(self, run_full=True):
+        """One pass of each schedule: recall against the exact per-layer top-k
+        (full routing), rerouted fractions, score-pair fraction."""
+        import numpy as np
+        import torch
+        w, rows, L = self.w, self.cfg.rows, self.w.n_layers
+        self.relay_step(keep_routes=True)
+        if run_full:
+            self.full_step()
+        torch.cuda.synchronize()
+        hit = tot = 0
+        for l in range(L):
+            a, b = self.relay_routes[l], self.full_routes[l]
+            eq = (a.unsqueeze(2) == b.unsqueeze(1)) & (a >= 0).unsqueeze(2)
+            hit += int(eq.any(1).sum().item())
+            tot += int((b >= 0).sum().item())
+        n_i = np.minimum(np.arange(w.n) + 1, w.n) if w.causal else np.full(w.n, w.n)
+        full_pairs_layer = int(n_i.sum()) * w.n_heads
+        rer = self.nrr.cpu().numpy().ravel()
+        relay_l = [l for l in range(L) if not w.is_anchor(l)]
+        anchors = L - len(relay_l)
+        return {
+            "recall": hit / tot,
+            "rerouted_frac_relay_layers": float(sum(rer[l] for l in relay_l)) / (rows * max(1, len(relay_l))),
+            "rerouted_frac_all_layers": float(anchors * rows + sum(rer[l] for l in relay_l)) / (rows * L),
+            "score_pair_frac": float(self.pairs.cpu().numpy().sum()) / (full_pairs_layer * L),
+            "mean_rerouted_rows": float(sum(rer[l] for l in relay_l)) / max(1, len(relay_l)),
+            "mean_n_i": float(n_i.mean()),
+            "full_pairs_layer": full_pairs_layer,
+        }
+
+    def tie_counts(self):
+        """Per layer, rows whose k-th and (k+1)-th best scores, or (k+m)-th and
+        (k+m+1)-th, lie within 1e-4 of the larger magnitude (the near-tie rule),
+        from the binary32 scores of full routing with k + m + 1 slots."""
+        import torch
+        w, cfg = self.w, self.cfg
+        K1 = w.k + w.m + 1
+        if K1 > 128 or K1 > w.n:
+            return None
+        c1 = dataclasses.replace(cfg, k=K1, m=0, r=0)
+        dev = self.full_routes.device
+        routes = torch.empty((cfg.rows, K1), dtype=torch.int32, device=dev)
+        sc = torch.empty((cfg.rows, K1), dtype=torch.float32, device=dev)
+        out = []
+        for l in range(w.n_layers):
+            self.rr.full_route(c1, self.Qd[l], self.Kd[l], routes, scores=sc)
+            srt = torch.sort(sc, dim=1, descending=True).values
+            ties = torch.zeros(cfg.rows, dtype=torch.bool, device=dev)
+            for a in (w.k - 1, w.k + w.m - 1):
+                x, y = srt[:, a], srt[:, a + 1]
+                band = 1e-4 * torch.maximum(x.abs(), y.abs())
+                ties |= torch.isfinite(y) & ((x - y) < band)
+            out.append(int(ties.sum().item()))
+        torch.cuda.synchronize()
+        return out
+
+    def close(self):
+        self.led.close()
+
+
+def measured_peaks(dev):
+    """Achievable rates on this GPU, beside the nominal peaks: a 1 GiB
+    device-to-device copy (bytes read + written per second) and an 8192^3
+    bf16 matrix product through torch (hipBLASLt)."""
+    import torch
+    out = {}
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device=dev)
+    b = torch.empty_like(a)
+    for _ in range(2):
+        b.copy_(a)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(10):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    out["copy_GBps"] = round(2 * n * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e9, 1)
+    del a, b
+    m = 8192
+    x = torch.randn((m, m), dtype=torch.bfloat16, device=dev)
+    y = torch.randn((m, m), dtype=torch.bfloat16, device=dev)
+    for _ in range(2):
+        z = x @ y
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(10):
+        z = x @ y
+    e1.record()
+    torch.cuda.synchronize()
+    out["gemm_bf16_TFLOPs"] = round(2.0 * m ** 3 * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e12, 1)
+    out["source"] = "torch device copy (1 GiB) and torch.matmul bf16 8192^3 (hipBLASLt)"
+    del x, y, z
+    torch.cuda.empty_cache()
+    return out
+
+
+def time_oracle(w, cpu_sample, heads, threads):
+    """The oracle over `heads` query heads (the first ones) for every layer,
+    with up to `threads` threads, one head per task (heads are independent).
+    Returns (seconds, threads used)."""
+    from concurrent.futures import ThreadPoolExecutor
+    import oracle
+    p = oracle.Problem(heads, max(1, heads // (w.n_heads // w.n_kv_heads)), w.n, w.n, w.d, w.k, w.m, w.r,
+                       w.causal, w.gamma, w.seed)
+    group = w.n_heads // w.n_kv_heads
+    sample = [(Qs[:heads], Ks[: max(1, heads // group)]) for Qs, Ks in cpu_sample]
+    ref = oracle.new_ledger(p)
+    head_rows = [list(range(h * w.n, (h + 1) * w.n)) for h in range(heads)]
+    import numpy as np
+    head_rows = [np.asarray(r, dtype=np.int64) for r in head_rows]
+
+    def one_head(rows):
+        for l, (Qs, Ks) in enumerate(sample):
+            if w.is_anchor(l):
+                oracle.anchor(p, l, Qs, Ks, ref, rows=rows)
+            else:
+                oracle.relay(p, l, Qs, Ks, ref, rows=rows)
+
+    used = max(1, min(threads, heads))
+    t0 = time.perf_counter()
+    if used == 1:
+        for r in head_rows:
+            one_head(r)
+    else:
+        with ThreadPoolExecutor(max_workers=used) as ex:
+            list(ex.map(one_head, head_rows))
+    return time.perf_counter() - t0, used
 
 
 def main():
@@ -134,108 +375,50 @@ def main():
     print(f"[bench] generating {describe(w)}", file=sys.stderr, flush=True)
 
     # ---- inputs, resident in HBM before any timing
-    hs = min(args.cpu_heads, w.n_heads)
+    cores = host_cores()
+    threads = args.cpu_threads or min(cores, 16)
     group = w.n_heads // w.n_kv_heads
-    hs = max(group, (hs // group) * group)
-    Qd, Kd, cpu_sample = [], [], []
-    for layer, Qf, Kf, Qx, Kx in synth.Generator(w):
-        Qd.append(rr.to_device(Qx, w.dtype, dev))
-        Kd.append(rr.to_device(Kx, w.dtype, dev))
-        if not args.no_cpu_baseline:
-            cpu_sample.append((np.ascontiguousarray(Qf[:hs]), np.ascontiguousarray(Kf[: hs // group])))
+    hs1 = max(group, (min(args.cpu_heads, w.n_heads) // group) * group)
+    hsn = max(hs1, (min(max(threads, hs1), w.n_heads) // group) * group)
+    Qd, Kd, cpu_sample = upload(w, dev, 0 if args.no_cpu_baseline else hsn)
     torch.cuda.synchronize()
     print("[bench] inputs resident", file=sys.stderr, flush=True)
 
-    led = rr.Ledger(cfg)
-    masks = torch.zeros((L, rows), dtype=torch.uint8, device=dev)
-    pairs = torch.zeros((L, 1), dtype=torch.int64, device=dev)
-    nrr = torch.zeros((L, 1), dtype=torch.int32, device=dev)
-    full_routes = torch.empty((L, rows, w.k), dtype=torch.int32, device=dev)
-    relay_routes = torch.empty((L, rows, w.k), dtype=torch.int32, device=dev)
-
-    def relay_step(keep_routes=False, marks=None):
-        for l in range(L):
-            if marks is not None:
-                marks[l].record()
-            out = relay_routes[l] if keep_routes else None
-            if w.is_anchor(l):
-                led.anchor(l, Qd[l], Kd[l], routes=out, pairs=pairs[l])
-            else:
-                led.relay(l, Qd[l], Kd[l], routes=out, mask=masks[l], pairs=pairs[l], n_rerouted=nrr[l])
-        if marks is not None:
-            marks[L].record()
-
-    def full_step():
-        for l in range(L):
-            rr.full_route(cfg, Qd[l], Kd[l], full_routes[l])
-
-    def timed(fn, steps):
-        torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        for _ in range(steps):
-            fn()
-        b.record()
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / steps
-
+    S = Schedule(w, cfg, Qd, Kd, dev)
     for _ in range(args.warmup):
-        relay_step()
+        S.relay_step()
         if not args.no_full:
-            full_step()
+            S.full_step()
     torch.cuda.synchronize()
     print("[bench] warm", file=sys.stderr, flush=True)
 
     # ---- timed region: the RouteRelay schedule, then the baseline
-    ms_step = timed(relay_step, args.steps)
-    ms_full = timed(full_step, args.steps) if not args.no_full else float("nan")
+    ms_step, per_step = S.timed(S.relay_step, args.steps)
+    ms_full, per_full = S.timed(S.full_step, args.steps) if not args.no_full else (float("nan"), [])
     print(f"[bench] relay step {ms_step:.3f} ms, full step {ms_full:.3f} ms", file=sys.stderr, flush=True)
 
     # ---- per-layer durations (events between library calls on the stream)
-    lay_ms = np.zeros(L)
-    for _ in range(args.steps):
-        marks = [torch.cuda.Event(enable_timing=True) for _ in range(L + 1)]
-        relay_step(marks=marks)
-        torch.cuda.synchronize()
-        lay_ms += [marks[l].elapsed_time(marks[l + 1]) for l in range(L)]
-    lay_ms /= args.steps
+    lay = S.layer_times(args.steps)
     anchor_l = [l for l in range(L) if w.is_anchor(l)]
     relay_l = [l for l in range(L) if not w.is_anchor(l)]
 
     # ---- per-kernel durations: library-recorded HIP events on the launch stream
     rr.profile_start()
     for _ in range(args.steps):
-        relay_step()
+        S.relay_step()
         if not args.no_full:
-            full_step()
+            S.full_step()
     prof = rr.profile_stop()
 
-    # ---- fidelity of one step (outside timing)
-    relay_step(keep_routes=True)
-    if args.no_full:
-        full_step()
-    torch.cuda.synchronize()
-    hit = tot = 0
-    for l in range(L):
-        a, b = relay_routes[l], full_routes[l]
-        va = a >= 0
-        eq = (a.unsqueeze(2) == b.unsqueeze(1)) & va.unsqueeze(2)
-        hit += int(eq.any(1).sum().item())
-        tot += int((b >= 0).sum().item())
-    recall = hit / tot
-    n_i = np.minimum(np.arange(w.n) + 1, w.n) if w.causal else np.full(w.n, w.n)
-    full_pairs_layer = int(n_i.sum()) * w.n_heads
-    pairs_np = pairs.cpu().numpy().ravel()
-    rer = nrr.cpu().numpy().ravel()
-    rer_relay = float(sum(rer[l] for l in relay_l)) / (rows * max(1, len(relay_l)))
-    rer_all = float(len(anchor_l) * rows + sum(rer[l] for l in relay_l)) / (rows * L)
-    pair_frac = float(pairs_np.sum()) / (full_pairs_layer * L)
+    # ---- fidelity of one step (outside timing), near ties
+    fid = S.fidelity(run_full=True)
+    ties = S.tie_counts()
+    print("[bench] fidelity and tie counts", file=sys.stderr, flush=True)
 
     # ---- roofline per kernel kind
     c = w.k + w.m + w.r
     kvb = w.n_kv_heads * w.n * w.d * e_bytes
-    mean_rerouted = float(sum(rer[l] for l in relay_l)) / max(1, len(relay_l))
-    mean_ni = float(n_i.mean())
+    mean_rerouted, mean_ni, full_pairs_layer = fid["mean_rerouted_rows"], fid["mean_n_i"], fid["full_pairs_layer"]
     mpeak = PEAK["mfma_bf16"] if w.dtype == "bf16" else PEAK["mfma_f32"]
     alg = {
         # per launch: (bound, algorithmic amount, unit, peak)
@@ -270,6 +453,8 @@ def main():
                 "unit": dk["unit"], "frac": dk["frac"],
                 "traffic": recorded_traffic(dom) if default_workload else None}
 
+    relay_ms = lay[:, relay_l].ravel() if relay_l else np.zeros(0)
+    anchor_ms = lay[:, anchor_l].ravel()
     value = rows * L / (ms_step * 1e-3)
     out = {
         "metric": "route rows/s per layer, RouteRelay anchor+relay schedule (vs GPU full routing)",
@@ -285,41 +470,115 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic",
         "config": {"workload": describe(w), "rows_per_layer": rows, "layers": L},
+        "step_ms_median": round(pct(per_step, 50), 4),
+        "step_ms_p10": round(pct(per_step, 10), 4),
+        "step_ms_p90": round(pct(per_step, 90), 4),
+        "value_at_median_step": round(rows * L / (pct(per_step, 50) * 1e-3), 1),
         "full_route_rows_per_s": round(rows * L / (ms_full * 1e-3), 1) if not args.no_full else None,
         "full_ms_per_step": round(ms_full, 4) if not args.no_full else None,
+        "full_step_ms_median": round(pct(per_full, 50), 4) if per_full else None,
         "speedup_vs_full": round(ms_full / ms_step, 3) if not args.no_full else None,
-        "relay_layer_rows_per_s": round(rows / (1e-3 * lay_ms[relay_l].mean()), 1) if relay_l else None,
-        "anchor_layer_rows_per_s": round(rows / (1e-3 * lay_ms[anchor_l].mean()), 1),
-        "relay_layer_us": round(1e3 * float(lay_ms[relay_l].mean()), 2) if relay_l else None,
-        "anchor_layer_us": round(1e3 * float(lay_ms[anchor_l].mean()), 2),
-        "recall": round(recall, 6),
-        "rerouted_frac_relay_layers": round(rer_relay, 4),
-        "rerouted_frac_all_layers": round(rer_all, 4),
-        "score_pair_frac": round(pair_frac, 4),
+        "relay_layer_rows_per_s": round(rows / (1e-3 * relay_ms.mean()), 1) if relay_l else None,
+        "relay_layer_rows_per_s_median": round(rows / (1e-3 * pct(relay_ms, 50)), 1) if relay_l else None,
+        "anchor_layer_rows_per_s": round(rows / (1e-3 * anchor_ms.mean()), 1),
+        "relay_layer_us": round(1e3 * float(relay_ms.mean()), 2) if relay_l else None,
+        "relay_layer_us_median_p10_p90": [round(1e3 * pct(relay_ms, q), 2) for q in (50, 10, 90)] if relay_l else None,
+        "anchor_layer_us": round(1e3 * float(anchor_ms.mean()), 2),
+        "anchor_layer_us_median_p10_p90": [round(1e3 * pct(anchor_ms, q), 2) for q in (50, 10, 90)],
+        "recall": round(fid["recall"], 6),
+        "rerouted_frac_relay_layers": round(fid["rerouted_frac_relay_layers"], 4),
+        "rerouted_frac_all_layers": round(fid["rerouted_frac_all_layers"], 4),
+        "score_pair_frac": round(fid["score_pair_frac"], 4),
+        "tie_rows_per_layer": ties,
+        "tie_rows_total": int(sum(ties)) if ties is not None else None,
         "kernel_ms_per_step": round(path_ms, 4),
         "kernels": kernels,
         "roofline": roofline,
     }
+    S.close()
+    del Qd, Kd
+    torch.cuda.empty_cache()
 
-    # ---- CPU baseline: the oracle, single-threaded, on a head subset
+    # ---- fidelity over seeds (the paper averages 3 to 10 seeds)
+    seeds = [int(x) for x in args.seeds.split(",") if x.strip()]
+    if seeds:
+        per_seed = {w.seed: fid}
+        for sd in seeds:
+            ws = w.with_(seed=sd)
+            print(f"[bench] fidelity, seed {sd}", file=sys.stderr, flush=True)
+            q, k_, _ = upload(ws, dev)
+            Ss = Schedule(ws, rr.Config.of(ws), q, k_, dev)
+            per_seed[sd] = Ss.fidelity(run_full=True)
+            Ss.close()
+            del q, k_
+            torch.cuda.empty_cache()
+        keys = ("recall", "rerouted_frac_relay_layers", "rerouted_frac_all_layers", "score_pair_frac")
+        out["fidelity_seeds"] = {"seeds": sorted(per_seed),
+                                 **{kk: round(float(np.mean([per_seed[s_][kk] for s_ in per_seed])), 6) for kk in keys},
+                                 "per_seed": {str(s_): {kk: round(per_seed[s_][kk], 6) for kk in keys} for s_ in sorted(per_seed)}}
+
+    # ---- low-drift operating points of the same shape (the method's regime)
+    pts = [float(x) for x in args.low_drift.split(",") if x.strip()]
+    if pts and args.rho is None:
+        low = []
+        for rho in pts:
+            wl = w.with_(rho=rho)
+            print(f"[bench] low-drift point rho={rho}", file=sys.stderr, flush=True)
+            q, k_, _ = upload(wl, dev)
+            cl = dataclasses.replace(rr.Config.of(wl), relay=args.relay)
+            Sl = Schedule(wl, cl, q, k_, dev)
+            Sl.relay_step()
+            Sl.full_step()
+            steps_l = max(3, min(args.steps, 5))
+            ms_l, _ = Sl.timed(Sl.relay_step, steps_l)
+            ms_f, _ = Sl.timed(Sl.full_step, steps_l)
+            lay_l = Sl.layer_times(steps_l)
+            rr.profile_start()
+            Sl.relay_step()
+            pr = rr.profile_stop()
+            fl = Sl.fidelity(run_full=True)
+            rel = lay_l[:, relay_l].ravel()
+            low.append({
+                "rho": rho,
+                "rerouted_frac_relay_layers": round(fl["rerouted_frac_relay_layers"], 4),
+                "recall": round(fl["recall"], 6),
+                "score_pair_frac": round(fl["score_pair_frac"], 4),
+                "relay_layer_rows_per_s": round(rows / (1e-3 * pct(rel, 50)), 1),
+                "full_route_rows_per_s": round(rows * L / (ms_f * 1e-3), 1),
+                "relay_vs_full_layer": round((ms_f / L) / pct(rel, 50), 3),
+                "schedule_rows_per_s": round(rows * L / (ms_l * 1e-3), 1),
+                "kernel_us": {k_: round(1e3 * t / n, 2) for k_, (t, n) in pr.items() if n},
+            })
+            Sl.close()
+            del q, k_
+            torch.cuda.empty_cache()
+        out["low_drift"] = low
+
+    # ---- measured peaks beside the nominal ones
+    mp = measured_peaks(dev)
+    out["measured_peaks"] = mp
+    ref_peak = mp["gemm_bf16_TFLOPs"] if dk["unit"] == "TFLOP/s" and w.dtype == "bf16" else (
+        mp["copy_GBps"] if dk["unit"] == "GB/s" else None)
+    if ref_peak:
+        out["roofline"]["frac_of_measured"] = round(dk["achieved"] / ref_peak, 4)
+
+    # ---- CPU baseline: the oracle on a head subset, on the host's cores and on one thread
     if not args.no_cpu_baseline:
-        import oracle
-        p = oracle.Problem(hs, hs // group, w.n, w.n, w.d, w.k, w.m, w.r, w.causal, w.gamma, w.seed)
-        ref = oracle.new_ledger(p)
-        t0 = time.perf_counter()
-        for l, (Qs, Ks) in enumerate(cpu_sample):
-            if w.is_anchor(l):
-                oracle.anchor(p, l, Qs, Ks, ref)
-            else:
-                oracle.relay(p, l, Qs, Ks, ref)
-        dt = time.perf_counter() - t0
+        model = cpu_model()
+        dt, used = time_oracle(w, cpu_sample, hsn, threads)
         out["cpu_baseline"] = {
-            "value": round(p.rows * L / dt, 1), "unit": "rows/s", "cores": 1, "kind": "oracle",
-            "sample": f"{hs} of {w.n_heads} query heads ({p.rows} rows) x {L} layers of the same "
-                      f"workload, binary64 C oracle, {dt:.1f} s",
+            "value": round(hsn * w.n * L / dt, 1), "unit": "rows/s", "cores": used, "kind": "oracle",
+            "sample": f"{hsn} of {w.n_heads} query heads ({hsn * w.n} rows) x {L} layers of the same workload, "
+                      f"binary64 C oracle, one head per thread, {used} threads, {dt:.1f} s",
+            "nproc": cores, "cpu_model": model,
+        }
+        dt1, _ = time_oracle(w, cpu_sample, hs1, 1)
+        out["cpu_baseline_1thread"] = {
+            "value": round(hs1 * w.n * L / dt1, 1), "unit": "rows/s", "cores": 1, "kind": "oracle",
+            "sample": f"{hs1} of {w.n_heads} query heads ({hs1 * w.n} rows) x {L} layers, one thread, {dt1:.1f} s",
+            "cpu_model": model,
         }
     print(json.dumps(out))
-    led.close()
 
 
 if __name__ == "__main__":
