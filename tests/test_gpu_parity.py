@@ -423,16 +423,18 @@ def test_state_errors():
 def test_sweep_cap_counts_unconverged_rows():
     """The collection loop's sweep cap lies above what the bisections need:
     with the default cap no row is counted.  With the cap lowered to one sweep
-    (a test hook) on inputs whose massive exact ties need repair sweeps, the
-    rows left unsettled are counted by rr_unconverged_rows, and their ledger
-    entries hold valid ids only (empty R and N, sentinels from the valid
-    chunks)."""
+    (a test hook), rows with all-zero queries -- every chunk ties at score 0,
+    so the first collection overflows and needs repair sweeps -- are left
+    unsettled: rr_unconverged_rows counts them, and their ledger entries hold
+    valid ids only (empty R and N, sentinels from the valid chunks), while
+    the other rows settle in one sweep and stay exact."""
     from parity_util import dev, ledger_np
     rr = rrmod()
     rng = np.random.default_rng(5)
-    H, n, d, k, m, r = 2, 300, 32, 24, 12, 8
-    Q = rng.integers(-2, 3, size=(H, n, d)).astype(np.float32)
-    K = rng.integers(-1, 2, size=(H, n, d)).astype(np.float32)
+    H, n, d, k, m, r = 2, 600, 64, 10, 5, 5
+    Q = (rng.standard_normal((H, n, d)) / 8).astype(np.float32)
+    Q[:, ::3] = 0.0
+    K = (rng.standard_normal((H, n, d)) / 8).astype(np.float32)
     cfg = rr.Config(H, H, n, n, d, k, m, r, "f32", False)
     note("sweep cap: default, then one sweep")
     before = rr.unconverged_rows()
@@ -454,6 +456,7 @@ def test_sweep_cap_counts_unconverged_rows():
     empty = (got["routes"] == -1).all(1)
     note(f"  unconverged rows at one sweep: {counted}")
     assert counted > 0 and counted == int(empty.sum())
+    assert empty.reshape(H, n)[:, ::3].all()
     assert ((got["sent"] >= -1) & (got["sent"] < n)).all()
     # rows that settled in one sweep are exact
     np.testing.assert_array_equal(got["routes"][~empty], ref["routes"][~empty])
