@@ -147,6 +147,27 @@ rr_status rr_relay_layer(rr_ledger *ledger, int32_t layer, const void *Qc, const
                          int32_t *routes, uint8_t *mask, int64_t *pairs, int32_t *n_rerouted,
                          void *hip_stream);
 
+/* Relay layer that allocates nothing, for callers that cannot allocate
+ * device memory at call time: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  The same computation and kernels as
+ * rr_relay_layer, on a ledger the caller owns, in the layout rr_ledger_export
+ * writes: led_routes [H_q*n_q, k], led_sent [H_q*n_q, m+r] (may be NULL when
+ * m + r = 0), led_build and led_age [H_q*n_q] int32, all device memory,
+ * updated in place.  The relay's scratch (flags, alpha / beta, per-workgroup
+ * partials, call totals, threshold seeds, a completion counter) lives in a
+ * static device area of the library, 4 MiB per GPU, held until the process
+ * ends; a configuration whose scratch exceeds it (beyond about 200 000 routed
+ * rows) returns RR_ERR_UNSUPPORTED before any work is enqueued.  There is no
+ * call-order state: the caller keeps layers non-decreasing after an anchor
+ * built the ledger.  Every call on one GPU shares that GPU's area, so calls
+ * that overlap on one GPU (concurrent streams or threads) race; calls
+ * ordered on one stream do not.  routes, mask, pairs and n_rerouted are as in
+ * rr_relay_layer. */
+rr_status rr_relay_layer_static(const rr_config *cfg, int32_t layer, const void *Qc, const void *Kc,
+                                int32_t *led_routes, int32_t *led_sent, int32_t *led_build,
+                                int32_t *led_age, int32_t *routes, uint8_t *mask, int64_t *pairs,
+                                int32_t *n_rerouted, void *hip_stream);
+
 /* Full routing baseline (Eq. (1)-(2)) with the same GEMM + TopK kernels and
  * no ledger: routes [H_q*n_q, cfg->k] int32 receives every row's route.
  * cfg->m and cfg->r are ignored.  route_scores (optional, [H_q*n_q, k]

@@ -33,8 +33,13 @@ struct rr_ledger {
 };
 
 // Device-resident library state, one copy per GPU: the running count of rows
-// whose selection stopped at the collection-sweep cap.
+// whose selection stopped at the collection-sweep cap, and the scratch area of
+// rr_relay_layer_static (relay flags, alpha / beta, per-workgroup partials,
+// call totals, threshold seeds, the one-pass completion counter).  Each GPU
+// the library runs on holds its own copy until the process ends.
+constexpr size_t kScratchBytes = (size_t)4 << 20;
 static __device__ unsigned long long g_unconverged_dev;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 namespace {
 
@@ -48,6 +53,7 @@ constexpr int kMaxDevices = 64;
 struct DeviceState {
     std::atomic<bool> ready{false};
     unsigned long long *unconverged = nullptr;
+    unsigned char *scratch = nullptr;
 };
 DeviceState g_devstate[kMaxDevices];
 std::mutex g_devstate_mu;
@@ -83,6 +89,12 @@ __global__ __launch_bounds__(kIdsThreads) void flagged_ids_kernel(const uint8_t 
         __syncthreads();
     }
     for (int j = base + (int)threadIdx.x; j < n_q; j += kIdsThreads) o[j] = -1;
+}
+
+// Zeroes n 32-bit words (one small launch).
+__global__ void clear_words_kernel(uint32_t *p, int n)
+{
+    for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0u;
 }
 
 rr_status fail(rr_status s, const std::string &msg)
@@ -240,6 +252,10 @@ rr_status device_state(DeviceState **out)
             e = hipGetSymbolAddress(&p, HIP_SYMBOL(g_unconverged_dev));
             if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress (unconverged-row counter)");
             st.unconverged = static_cast<unsigned long long *>(p);
+            p = nullptr;
+            e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+            if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress (relay scratch)");
+            st.scratch = static_cast<unsigned char *>(p);
             st.ready.store(true, std::memory_order_release);
         }
     }
@@ -267,6 +283,191 @@ rr::RouteArgs route_args(const rr_config &c, const void *Q, const void *K)
     a.tiles_per_head = (c.n_q + a.tile_rows - 1) / a.tile_rows;
     a.seed = c.seed;
     return a;
+}
+
+// Schedule of a relay layer for a configuration: one pass where a tile's
+// ledger bitmaps fit its LDS -- by default unless the inputs are non-causal
+// and the rescoring would use dense tiles, whose threshold seeds make the
+// split schedule faster there -- and, for the split schedule with dense
+// rescoring, whether the rescoring pass leaves threshold seeds.
+struct RelayPlan {
+    bool fused, seeds;
+    int bm_words;
+    rr::RescoreGeometry geo;
+};
+
+RelayPlan relay_plan(const rr_config &c)
+{
+    RelayPlan p;
+    p.bm_words = relay_bm_words(c.n_k);
+    const bool fits = p.bm_words <= rr::route_relay_max_bm_words(c.dtype, c.d, c.k + c.m);
+    rr::rescore_geometry(rows_of(c), c.n_q, c.n_k, p.geo);
+    p.fused = fits && ((c.options & RR_OPT_ONE_PASS_RELAY) ||
+                       (!(c.options & RR_OPT_SPLIT_RELAY) && (c.causal || !p.geo.dense)));
+    p.seeds = !p.fused && p.geo.dense && rr::rescore_dense_seeds(c.dtype, c.d);
+    return p;
+}
+
+// Per-workgroup partial slots a relay layer needs: one per rescoring
+// workgroup (split) or per route tile (one pass).
+int64_t relay_partial_slots(const rr_config &c)
+{
+    const int64_t rescore = (int64_t)c.n_heads * ((c.n_q + rr::kRescoreWaves - 1) / rr::kRescoreWaves);
+    const int tile = rr::route_tile_rows(c.k + c.m, c.n_heads, c.n_q);
+    const int64_t tiles = (int64_t)c.n_heads * ((c.n_q + tile - 1) / tile);
+    return rescore > tiles ? rescore : tiles;
+}
+
+// Byte offsets of the relay scratch inside the static area (each 256-byte
+// aligned) and the bytes it takes.
+struct StaticLayout {
+    size_t done, stat_pairs, stat_nrr, blk_pairs, blk_count, flags, alpha, beta, seed_bound, seed_rmax, bytes;
+};
+
+StaticLayout static_layout(const rr_config &c, const RelayPlan &p)
+{
+    const size_t rows = (size_t)rows_of(c), slots = (size_t)relay_partial_slots(c);
+    StaticLayout l;
+    size_t at = 0;
+    auto take = [&](size_t bytes) {
+        const size_t o = at;
+        at = (at + bytes + 255) & ~(size_t)255;
+        return o;
+    };
+    l.done = take(sizeof(uint32_t));
+    l.stat_pairs = take(sizeof(int64_t));
+    l.stat_nrr = take(sizeof(int32_t));
+    l.blk_pairs = take(slots * sizeof(int64_t));
+    l.blk_count = take(slots * sizeof(int32_t));
+    l.flags = take(rows);
+    l.alpha = take(rows * sizeof(float));
+    l.beta = take(rows * sizeof(float));
+    l.seed_bound = p.seeds ? take(rows * sizeof(float)) : 0;
+    l.seed_rmax = p.seeds ? take(rows * sizeof(float)) : 0;
+    l.bytes = at;
+    return l;
+}
+
+// Device buffers of one relay layer: the ledger and the relay scratch.
+struct RelayBuffers {
+    int32_t *routes = nullptr, *sent = nullptr, *build = nullptr, *age = nullptr;
+    uint8_t *flags = nullptr;
+    float *alpha = nullptr, *beta = nullptr;
+    float *seed_bound = nullptr, *seed_rmax = nullptr;  // split + dense rescoring: threshold seeds (or null)
+    int64_t *blk_pairs = nullptr;                       // per-workgroup partials
+    int32_t *blk_count = nullptr;
+    int64_t *stat_pairs = nullptr;
+    int32_t *stat_nrr = nullptr;
+    uint32_t *done = nullptr;  // one pass: finished-workgroup counter (zero between launches)
+    bool fused = false;
+    int32_t bm_words = 0;
+    unsigned long long *unconverged = nullptr;
+};
+
+// Enqueues one relay layer (Sec. 3.2; Sec. 4.1-4.2) on `stream`: the one
+// pass, or rescoring + trigger then the reroute of the flagged rows
+// compacted per head.  `profile`: bracket the launches with the profiler's
+// events when profiling is on.
+rr_status relay_launch(const rr_config &c, const RelayBuffers &b, int32_t layer, const void *Qc, const void *Kc,
+                       int32_t *routes, uint8_t *mask, int64_t *pairs, int32_t *n_rerouted, hipStream_t stream,
+                       bool profile)
+{
+    auto launch = [&](int kind, auto fn) { return profile ? timed(kind, stream, fn) : fn(); };
+    if (b.fused) {
+        // one pass: each tile rescores its rows' ledgers on its own scores,
+        // flags them, and routes the flagged rows into the ledger
+        rr::RouteArgs a = route_args(c, Qc, Kc);
+        a.unconverged = b.unconverged;
+        a.layer = layer;
+        a.mode = rr::MODE_RELAY;
+        a.led_routes = b.routes;
+        a.led_sent = b.sent;
+        a.led_build = b.build;
+        a.led_age = b.age;
+        a.flags = b.flags;
+        a.mask_out = mask;
+        a.alpha_out = b.alpha;
+        a.beta_out = b.beta;
+        a.gamma = c.gamma;
+        a.bm_words = b.bm_words;
+        a.blk_pairs = b.blk_pairs;
+        a.blk_count = b.blk_count;
+        a.done = b.done;
+        a.stat_pairs = b.stat_pairs;
+        a.stat_nrr = b.stat_nrr;
+        a.pairs_out = pairs;
+        a.nrr_out = n_rerouted;
+        const int grid = c.n_heads * a.tiles_per_head;
+        hipError_t e = launch(RR_KERNEL_RELAY, [&] { return rr::launch_route(a, c.dtype, grid, stream); });
+        if (e != hipSuccess) return hip_fail(e, "relay launch");
+    } else {
+        rr::RescoreArgs s;
+        std::memset(&s, 0, sizeof(s));
+        s.Q = Qc;
+        s.K = Kc;
+        s.n_heads = c.n_heads;
+        s.n_kv_heads = c.n_kv_heads;
+        s.n_q = c.n_q;
+        s.n_k = c.n_k;
+        s.d = c.d;
+        s.k = c.k;
+        s.m = c.m;
+        s.r = c.r;
+        s.causal = c.causal;
+        s.layer = layer;
+        rr::RescoreGeometry geo;
+        rr::rescore_geometry(rows_of(c), c.n_q, c.n_k, geo);
+        s.blocks_per_head = geo.blocks_per_head;
+        s.rows_per_wave = geo.rows_per_wave;
+        s.rows_per_block = geo.rows_per_block;
+        s.dense = geo.dense ? 1 : 0;
+        s.bm_words = geo.bm_words;
+        s.gamma = c.gamma;
+        s.led_routes = b.routes;
+        s.led_sent = b.sent;
+        s.led_build = b.build;
+        s.led_age = b.age;
+        s.flags = b.flags;
+        s.mask_out = mask;
+        s.alpha = b.alpha;
+        s.beta = b.beta;
+        s.blk_pairs = b.blk_pairs;
+        s.blk_count = b.blk_count;
+        s.seed_bound = b.seed_bound;
+        s.seed_rmax = b.seed_rmax;
+        hipError_t e = launch(RR_KERNEL_RESCORE, [&] { return rr::launch_rescore(s, c.dtype, stream); });
+        if (e != hipSuccess) return hip_fail(e, "rescore launch");
+
+        rr::RouteArgs a = route_args(c, Qc, Kc);
+        a.unconverged = b.unconverged;
+        a.layer = layer;
+        a.mode = rr::MODE_REROUTE;
+        a.led_routes = b.routes;
+        a.led_sent = b.sent;
+        a.led_build = b.build;
+        a.led_age = b.age;
+        a.flags = b.flags;
+        a.blk_count = b.blk_count;
+        a.blk_pairs = b.blk_pairs;
+        a.rescore_bph = geo.blocks_per_head;
+        a.stat_pairs = b.stat_pairs;
+        a.stat_nrr = b.stat_nrr;
+        a.pairs_out = pairs;
+        a.nrr_out = n_rerouted;
+        a.seed_bound = b.seed_bound;
+        a.seed_rmax = b.seed_rmax;
+        const int max_tiles = c.n_heads * a.tiles_per_head;
+        const int grid8 = (max_tiles + 7) & ~7;  // a multiple of 8: per-XCD tile ranges
+        const int grid = grid8 < 1024 ? grid8 : 1024;
+        e = launch(RR_KERNEL_REROUTE, [&] { return rr::launch_route(a, c.dtype, grid, stream); });
+        if (e != hipSuccess) return hip_fail(e, "reroute launch");
+    }
+    if (routes) {
+        hipError_t e = hipMemcpyAsync(routes, b.routes, sizeof(int32_t) * rows_of(c) * c.k, hipMemcpyDeviceToDevice,
+                                      stream);
+        if (e != hipSuccess) return hip_fail(e, "route copy");
+    }
+    return RR_OK;
 }
 
 }  // namespace
@@ -311,8 +512,8 @@ rr_status rr_ledger_create(const rr_config *cfg, rr_ledger **out)
         return fail(RR_ERR_HIP, "hipGetDevice failed");
     }
     const int64_t rows = L->rows;
-    // rescoring workgroups: at most one per kRescoreWaves rows of a head
-    const int64_t max_blocks = (int64_t)cfg->n_heads * ((cfg->n_q + rr::kRescoreWaves - 1) / rr::kRescoreWaves);
+    // per-workgroup partial slots of a relay layer
+    const int64_t max_blocks = relay_partial_slots(*cfg);
     if ((st = alloc(&L->routes, rows * cfg->k, "routes")) != RR_OK ||
         (st = alloc(&L->sent, rows * (cfg->m + cfg->r), "sentinels")) != RR_OK ||
         (st = alloc(&L->build, rows, "build")) != RR_OK || (st = alloc(&L->age, rows, "age")) != RR_OK ||
@@ -326,20 +527,14 @@ rr_status rr_ledger_create(const rr_config *cfg, rr_ledger **out)
         delete L;
         return st;
     }
-    // relay layers in one pass where a tile's ledger bitmaps (R and C words
-    // over the padded key range, odd row stride) fit its LDS -- by default
-    // unless the inputs are non-causal and the rescoring would use dense
-    // tiles, whose threshold seeds make the split schedule faster there
-    L->bm_words = relay_bm_words(cfg->n_k);
-    const bool fits = L->bm_words <= rr::route_relay_max_bm_words(cfg->dtype, cfg->d, cfg->k + cfg->m);
-    rr::RescoreGeometry geo;
-    rr::rescore_geometry(rows, cfg->n_q, cfg->n_k, geo);
-    L->fused = fits && ((cfg->options & RR_OPT_ONE_PASS_RELAY) ||
-                        (!(cfg->options & RR_OPT_SPLIT_RELAY) && (cfg->causal || !geo.dense)));
+    // the relay schedule (one pass or split) and the split schedule's
+    // threshold seeds
+    const RelayPlan plan = relay_plan(*cfg);
+    L->bm_words = plan.bm_words;
+    L->fused = plan.fused;
     if ((L->fused && (st = alloc(&L->done, 1, "relay counter")) != RR_OK) ||
-        (!L->fused && geo.dense && rr::rescore_dense_seeds(cfg->dtype, cfg->d) &&
-         ((st = alloc(&L->seed_bound, rows, "seed bounds")) != RR_OK ||
-          (st = alloc(&L->seed_rmax, rows, "seed maxima")) != RR_OK))) {
+        (plan.seeds && ((st = alloc(&L->seed_bound, rows, "seed bounds")) != RR_OK ||
+                        (st = alloc(&L->seed_rmax, rows, "seed maxima")) != RR_OK))) {
         free_all(L);
         delete L;
         return st;
@@ -413,104 +608,80 @@ rr_status rr_relay_layer(rr_ledger *L, int32_t layer, const void *Qc, const void
     DeviceState *ds = nullptr;
     rr_status st = device_state(&ds);
     if (st != RR_OK) return st;
-    const rr_config &c = L->cfg;
-    hipStream_t stream = reinterpret_cast<hipStream_t>(hip_stream);
-
-    if (L->fused) {
-        // one pass: each tile rescores its rows' ledgers on its own scores,
-        // flags them, and routes the flagged rows into the ledger
-        rr::RouteArgs a = route_args(c, Qc, Kc);
-        a.unconverged = ds->unconverged;
-        a.layer = layer;
-        a.mode = rr::MODE_RELAY;
-        a.led_routes = L->routes;
-        a.led_sent = L->sent;
-        a.led_build = L->build;
-        a.led_age = L->age;
-        a.flags = L->flags;
-        a.mask_out = mask;
-        a.alpha_out = L->alpha;
-        a.beta_out = L->beta;
-        a.gamma = c.gamma;
-        a.bm_words = L->bm_words;
-        a.blk_pairs = L->blk_pairs;
-        a.blk_count = L->blk_count;
-        a.done = L->done;
-        a.stat_pairs = L->stat_pairs;
-        a.stat_nrr = L->stat_nrr;
-        a.pairs_out = pairs;
-        a.nrr_out = n_rerouted;
-        const int grid = c.n_heads * a.tiles_per_head;
-        hipError_t e = timed(RR_KERNEL_RELAY, stream, [&] { return rr::launch_route(a, c.dtype, grid, stream); });
-        if (e != hipSuccess) return hip_fail(e, "relay launch");
-    } else {
-        rr::RescoreArgs s;
-        std::memset(&s, 0, sizeof(s));
-        s.Q = Qc;
-        s.K = Kc;
-        s.n_heads = c.n_heads;
-        s.n_kv_heads = c.n_kv_heads;
-        s.n_q = c.n_q;
-        s.n_k = c.n_k;
-        s.d = c.d;
-        s.k = c.k;
-        s.m = c.m;
-        s.r = c.r;
-        s.causal = c.causal;
-        s.layer = layer;
-        rr::RescoreGeometry geo;
-        rr::rescore_geometry(L->rows, c.n_q, c.n_k, geo);
-        s.blocks_per_head = geo.blocks_per_head;
-        s.rows_per_wave = geo.rows_per_wave;
-        s.rows_per_block = geo.rows_per_block;
-        s.dense = geo.dense ? 1 : 0;
-        s.bm_words = geo.bm_words;
-        s.gamma = c.gamma;
-        s.led_routes = L->routes;
-        s.led_sent = L->sent;
-        s.led_build = L->build;
-        s.led_age = L->age;
-        s.flags = L->flags;
-        s.mask_out = mask;
-        s.alpha = L->alpha;
-        s.beta = L->beta;
-        s.blk_pairs = L->blk_pairs;
-        s.blk_count = L->blk_count;
-        s.seed_bound = L->seed_bound;
-        s.seed_rmax = L->seed_rmax;
-        hipError_t e = timed(RR_KERNEL_RESCORE, stream, [&] { return rr::launch_rescore(s, c.dtype, stream); });
-        if (e != hipSuccess) return hip_fail(e, "rescore launch");
-
-        rr::RouteArgs a = route_args(c, Qc, Kc);
-        a.unconverged = ds->unconverged;
-        a.layer = layer;
-        a.mode = rr::MODE_REROUTE;
-        a.led_routes = L->routes;
-        a.led_sent = L->sent;
-        a.led_build = L->build;
-        a.led_age = L->age;
-        a.flags = L->flags;
-        a.blk_count = L->blk_count;
-        a.blk_pairs = L->blk_pairs;
-        a.rescore_bph = geo.blocks_per_head;
-        a.stat_pairs = L->stat_pairs;
-        a.stat_nrr = L->stat_nrr;
-        a.pairs_out = pairs;
-        a.nrr_out = n_rerouted;
-        a.seed_bound = L->seed_bound;
-        a.seed_rmax = L->seed_rmax;
-        const int max_tiles = c.n_heads * a.tiles_per_head;
-        const int grid8 = (max_tiles + 7) & ~7;  // a multiple of 8: per-XCD tile ranges
-        const int grid = grid8 < 1024 ? grid8 : 1024;
-        e = timed(RR_KERNEL_REROUTE, stream, [&] { return rr::launch_route(a, c.dtype, grid, stream); });
-        if (e != hipSuccess) return hip_fail(e, "reroute launch");
-    }
-    if (routes) {
-        hipError_t e = hipMemcpyAsync(routes, L->routes, sizeof(int32_t) * L->rows * c.k, hipMemcpyDeviceToDevice, stream);
-        if (e != hipSuccess) return hip_fail(e, "route copy");
-    }
+    RelayBuffers b;
+    b.routes = L->routes;
+    b.sent = L->sent;
+    b.build = L->build;
+    b.age = L->age;
+    b.flags = L->flags;
+    b.alpha = L->alpha;
+    b.beta = L->beta;
+    b.seed_bound = L->seed_bound;
+    b.seed_rmax = L->seed_rmax;
+    b.blk_pairs = L->blk_pairs;
+    b.blk_count = L->blk_count;
+    b.stat_pairs = L->stat_pairs;
+    b.stat_nrr = L->stat_nrr;
+    b.done = L->done;
+    b.fused = L->fused;
+    b.bm_words = L->bm_words;
+    b.unconverged = ds->unconverged;
+    st = relay_launch(L->cfg, b, layer, Qc, Kc, routes, mask, pairs, n_rerouted,
+                      reinterpret_cast<hipStream_t>(hip_stream), true);
+    if (st != RR_OK) return st;
     L->last_layer = layer;
     return RR_OK;
+}
+
+rr_status rr_relay_layer_static(const rr_config *cfg, int32_t layer, const void *Qc, const void *Kc,
+                                int32_t *led_routes, int32_t *led_sent, int32_t *led_build, int32_t *led_age,
+                                int32_t *routes, uint8_t *mask, int64_t *pairs, int32_t *n_rerouted,
+                                void *hip_stream)
+{
+    rr_status st = validate(cfg, true);
+    if (st != RR_OK) return st;
+    const rr_config &c = *cfg;
+    if (!Qc || !Kc || !led_routes || !led_build || !led_age || (!led_sent && c.m + c.r > 0))
+        return fail(RR_ERR_INVALID, "Qc, Kc and the ledger arrays (routes, sent, build, age) are required");
+    if (layer < 0) return fail(RR_ERR_INVALID, "layer must be >= 0");
+    RelayPlan plan = relay_plan(c);
+    const StaticLayout lay = static_layout(c, plan);
+    if (lay.bytes > kScratchBytes)
+        return fail(RR_ERR_UNSUPPORTED, "rr_relay_layer_static: the relay scratch of this configuration (" +
+                                            std::to_string(lay.bytes) + " bytes) exceeds the library's " +
+                                            std::to_string(kScratchBytes) + "-byte static area");
+    DeviceState *ds = nullptr;
+    if ((st = device_state(&ds)) != RR_OK) return st;
+    unsigned char *base = ds->scratch;
+    RelayBuffers b;
+    b.routes = led_routes;
+    b.sent = led_sent;
+    b.build = led_build;
+    b.age = led_age;
+    b.done = reinterpret_cast<uint32_t *>(base + lay.done);
+    b.stat_pairs = reinterpret_cast<int64_t *>(base + lay.stat_pairs);
+    b.stat_nrr = reinterpret_cast<int32_t *>(base + lay.stat_nrr);
+    b.blk_pairs = reinterpret_cast<int64_t *>(base + lay.blk_pairs);
+    b.blk_count = reinterpret_cast<int32_t *>(base + lay.blk_count);
+    b.flags = base + lay.flags;
+    b.alpha = reinterpret_cast<float *>(base + lay.alpha);
+    b.beta = reinterpret_cast<float *>(base + lay.beta);
+    b.seed_bound = plan.seeds ? reinterpret_cast<float *>(base + lay.seed_bound) : nullptr;
+    b.seed_rmax = plan.seeds ? reinterpret_cast<float *>(base + lay.seed_rmax) : nullptr;
+    b.fused = plan.fused;
+    b.bm_words = plan.bm_words;
+    b.unconverged = ds->unconverged;
+    hipStream_t stream = reinterpret_cast<hipStream_t>(hip_stream);
+    if (plan.fused) {
+        // the one pass's completion counter must read zero at launch: the
+        // area keeps the previous call's contents, so it is cleared here, on
+        // the caller's stream, by a kernel (a stream under capture records a
+        // plain kernel node, not a memset)
+        hipLaunchKernelGGL(clear_words_kernel, dim3(1), dim3(64), 0, stream, b.done, 1);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return hip_fail(e, "relay scratch clear");
+    }
+    return relay_launch(c, b, layer, Qc, Kc, routes, mask, pairs, n_rerouted, stream, false);
 }
 
 rr_status rr_full_route(const rr_config *cfg, const void *Qc, const void *Kc, int32_t *routes, float *route_scores,

@@ -24,7 +24,7 @@ EXPORTED = (
     "rr_ledger_create", "rr_ledger_destroy", "rr_anchor_route", "rr_relay_layer", "rr_full_route",
     "rr_ledger_routes", "rr_ledger_export", "rr_ledger_import", "rr_ledger_relay_stats",
     "rr_ledger_index_bytes", "rr_status_string", "rr_last_error", "rr_profile_start",
-    "rr_profile_stop", "rr_unconverged_rows", "rr_set_sweep_cap",
+    "rr_profile_stop", "rr_unconverged_rows", "rr_set_sweep_cap", "rr_relay_layer_static",
 )
 KERNEL_KINDS = ("full", "anchor", "reroute", "rescore", "relay")
 
@@ -66,6 +66,7 @@ def _load():
         "rr_profile_stop": (ctypes.c_int, [vp, vp, i32]),
         "rr_unconverged_rows": (ctypes.c_int, [ctypes.POINTER(ctypes.c_uint64)]),
         "rr_set_sweep_cap": (ctypes.c_int, [i32]),
+        "rr_relay_layer_static": (ctypes.c_int, [cfgp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -186,6 +187,21 @@ def full_route(cfg: Config, Q, K, routes, scores=None, pairs=None, stream=None):
     _check(lib.rr_full_route(ctypes.byref(cfg.c()), q, k, _out(routes, (cfg.rows, cfg.k), torch.int32),
                              _out(scores, (cfg.rows, cfg.k), torch.float32),
                              _out(pairs, (1,), torch.int64), _stream(stream)))
+
+
+def relay_static(cfg: Config, layer: int, Q, K, ledger, routes=None, mask=None, pairs=None, n_rerouted=None,
+                 stream=None):
+    """rr_relay_layer_static: a relay layer on a caller-owned ledger (a dict of
+    int32 device tensors as Ledger.export returns), updated in place; the
+    library allocates nothing."""
+    q, k = _inputs(cfg, Q, K)
+    c = cfg
+    _check(lib.rr_relay_layer_static(
+        ctypes.byref(cfg.c()), layer, q, k, _out(ledger["routes"], (c.rows, c.k), torch.int32),
+        _out(ledger["sent"], (c.rows, c.m + c.r), torch.int32) if c.m + c.r else None,
+        _out(ledger["build"], (c.rows,), torch.int32), _out(ledger["age"], (c.rows,), torch.int32),
+        _out(routes, (c.rows, c.k), torch.int32), _out(mask, (c.rows,), torch.uint8),
+        _out(pairs, (1,), torch.int64), _out(n_rerouted, (1,), torch.int32), _stream(stream)))
 
 
 class Ledger:
