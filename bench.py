@@ -81,6 +81,9 @@ def parse():
     ap.add_argument("--no-full", action="store_true", help="skip the full-routing baseline")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a device-to-device copy of MIB MiB (calibrates the HBM byte counters)")
+    ap.add_argument("--counter-pass", default="", choices=("", "full", "anchor", "relay"),
+                    help="only launch this call 5 times on the workload's first layers (a program for "
+                         "rocprofv3 counter passes) and exit")
     ap.add_argument("--low-drift", default="0.005,0.01,0.02",
                     help="extra operating points: comma-separated rho values of the same shape ('' for none)")
     ap.add_argument("--seeds", default="1,2", help="extra seeds for the fidelity average ('' for none)")
@@ -371,6 +374,25 @@ def main():
     w = synth.preset(args.workload, **kw)
     cfg = dataclasses.replace(rr.Config.of(w), relay=args.relay)
     rows, L = cfg.rows, w.n_layers
+    if args.counter_pass:
+        # five launches of one call on the first two layers, nothing else
+        lay = synth.layers(w.with_(n_layers=2))
+        Q = [rr.to_device(x[2], w.dtype, dev) for x in lay]
+        K = [rr.to_device(x[3], w.dtype, dev) for x in lay]
+        led = rr.Ledger(cfg)
+        out = torch.empty((rows, w.k), dtype=torch.int32, device=dev)
+        for _ in range(5):
+            if args.counter_pass == "full":
+                rr.full_route(cfg, Q[1], K[1], out)
+            elif args.counter_pass == "anchor":
+                led.anchor(0, Q[0], K[0])
+            else:
+                led.anchor(0, Q[0], K[0])
+                led.relay(1, Q[1], K[1])
+        torch.cuda.synchronize()
+        led.close()
+        print(json.dumps({"counter_pass": args.counter_pass, "launches": 5}))
+        return
     e_bytes = 2 if w.dtype == "bf16" else 4
     print(f"[bench] generating {describe(w)}", file=sys.stderr, flush=True)
 
