@@ -84,6 +84,10 @@ def parse():
     ap.add_argument("--counter-pass", default="", choices=("", "full", "anchor", "relay"),
                     help="only launch this call 5 times on the workload's first layers (a program for "
                          "rocprofv3 counter passes) and exit")
+    ap.add_argument("--study", default="", choices=("", "ablation", "stride"),
+                    help="run a fidelity study instead of the benchmark: the sentinel ablation (Table 3 "
+                         "shape) or RouteRelay against a fixed refresh stride of 4 (Table 2 shape)")
+    ap.add_argument("--study-seeds", type=int, default=0, help="seeds of a study (0: 5 for ablation, 10 for stride)")
     ap.add_argument("--low-drift", default="0.005,0.01,0.02",
                     help="extra operating points: comma-separated rho values of the same shape ('' for none)")
     ap.add_argument("--seeds", default="1,2", help="extra seeds for the fidelity average ('' for none)")
@@ -115,7 +119,8 @@ def host_cores() -> int:
 
 
 def describe(w) -> str:
-    parts = [f"{w.name}: {w.n_heads} query heads / {w.n_kv_heads} key heads x {w.n} chunks",
+    keys = f"{w.n} chunks" if w.nk == w.n else f"{w.n} query chunks, {w.nk} key chunks"
+    parts = [f"{w.name}: {w.n_heads} query heads / {w.n_kv_heads} key heads x {keys}",
              f"d={w.d} {w.dtype}", f"k={w.k} m={w.m} r={w.r}",
              f"{w.n_layers} layers, anchor every {w.anchor_every or w.n_layers}",
              f"{w.clusters} clusters, rho={w.rho}"]
@@ -335,6 +340,82 @@ def time_oracle(w, cpu_sample, heads, threads):
     return time.perf_counter() - t0, used
 
 
+def run_policy(w, dev, policy="relay", stride=4):
+    """One seeded run of a workload through the library: RouteRelay (anchor at
+    layer 0, relay layers after it) or a fixed refresh stride (full routing
+    into the ledger every `stride` layers, the routes reused unchanged in
+    between, no rescoring).  Returns recall against the exact per-layer top-k,
+    the rerouted-row fraction over all layers (anchor rows counted as routed,
+    as Tables 2-3 count them) and the score-pair fraction of full routing."""
+    import numpy as np  # noqa: F401
+    import torch
+    from paper_2609_07306_amd import routerelay as rr
+    from paper_2609_07306_amd import synth
+    cfg = rr.Config.of(w)
+    led = rr.Ledger(cfg)
+    rows, L = cfg.rows, w.n_layers
+    exact = torch.empty((rows, w.k), dtype=torch.int32, device=dev)
+    mask = torch.empty(rows, dtype=torch.uint8, device=dev)
+    pairs = torch.zeros(1, dtype=torch.int64, device=dev)
+    full_pairs = torch.zeros(1, dtype=torch.int64, device=dev)
+    hit = tot = rer = sp = fp = 0
+    for l, _, _, Qx, Kx in synth.Generator(w):
+        Q, K = rr.to_device(Qx, w.dtype, dev), rr.to_device(Kx, w.dtype, dev)
+        rr.full_route(cfg, Q, K, exact, pairs=full_pairs)
+        if l == 0 or (policy == "stride" and l % stride == 0):
+            led.anchor(l, Q, K, pairs=pairs)
+            rer += rows
+            sp += int(pairs.item())
+        elif policy == "relay":
+            led.relay(l, Q, K, mask=mask, pairs=pairs)
+            rer += int(mask.sum().item())
+            sp += int(pairs.item())
+        got = torch.empty((rows, w.k), dtype=torch.int32, device=dev)
+        got.copy_(led.export()["routes"])
+        eq = (got.unsqueeze(2) == exact.unsqueeze(1)) & (got >= 0).unsqueeze(2)
+        hit += int(eq.any(1).sum().item())
+        tot += int((exact >= 0).sum().item())
+        fp += int(full_pairs.item())
+    led.close()
+    return {"recall": hit / tot, "rerouted": rer / (rows * L), "score_pairs": sp / fp}
+
+
+def study(args, dev):
+    """Fidelity studies of the paper's Sec. 5 on this build's generator:
+    the sentinel ablation (Sec. 5.2, Table 3 shape) and RouteRelay against a
+    fixed refresh stride (Sec. 5.1, Table 2 shape); means over seeds."""
+    import numpy as np
+    from paper_2609_07306_amd import synth
+    if args.study == "ablation":
+        seeds = args.study_seeds or 5
+        base = synth.preset("ablation")
+        if args.rho is not None:
+            base = base.with_(rho=args.rho)
+        points = [("random only", 0, 12), ("near-miss only (12)", 12, 0), ("near-miss only (24)", 24, 0),
+                  ("12 near-miss + 12 random", 12, 12), ("24 near-miss + 12 random", 24, 12),
+                  ("48 near-miss + 12 random", 48, 12)]
+        out = []
+        for name, m, r in points:
+            res = [run_policy(base.with_(m=m, r=r, seed=sd), dev) for sd in range(seeds)]
+            out.append({"sentinels": name, "m": m, "r": r,
+                        **{k: round(100 * float(np.mean([x[k] for x in res])), 3) for k in res[0]}})
+            print(f"[study] {name}: {out[-1]}", file=sys.stderr, flush=True)
+        return {"study": "sentinel ablation (Table 3 shape)", "workload": describe(base), "seeds": seeds,
+                "units": "percent", "points": out}
+    seeds = args.study_seeds or 10
+    base = synth.preset("stride")
+    rhos = [args.rho] if args.rho is not None else [0.05, 0.2, 0.3]
+    out = []
+    for rho in rhos:
+        for policy in ("stride", "relay"):
+            res = [run_policy(base.with_(rho=rho, seed=sd), dev, policy) for sd in range(seeds)]
+            out.append({"rho": rho, "policy": "fixed stride 4" if policy == "stride" else "RouteRelay",
+                        **{k: round(100 * float(np.mean([x[k] for x in res])), 3) for k in res[0]}})
+            print(f"[study] {out[-1]}", file=sys.stderr, flush=True)
+    return {"study": "RouteRelay vs fixed refresh stride 4 (Table 2 shape)", "workload": describe(base),
+            "seeds": seeds, "units": "percent", "points": out}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -364,6 +445,10 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": n}))
+        return
+
+    if args.study:
+        print(json.dumps(study(args, dev)))
         return
 
     kw = {}

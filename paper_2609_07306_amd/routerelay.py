@@ -116,7 +116,7 @@ class Config:
     @staticmethod
     def of(w) -> "Config":
         """From a synth.Workload."""
-        return Config(w.n_heads, w.n_kv_heads, w.n, w.n, w.d, w.k, w.m, w.r, w.dtype, w.causal,
+        return Config(w.n_heads, w.n_kv_heads, w.n, w.nk, w.d, w.k, w.m, w.r, w.dtype, w.causal,
                       w.gamma, w.seed)
 
 

@@ -52,11 +52,16 @@ class Workload:
     near_ties: bool = False
     seed: int = 0
     gamma: float = 0.0
+    n_keys: int = 0            # key chunks n_k when it differs from n_q = n (0: n_k = n)
     extra: dict = field(default_factory=dict, compare=False)
 
     @property
     def rows(self) -> int:
         return self.n_heads * self.n
+
+    @property
+    def nk(self) -> int:
+        return self.n_keys or self.n
 
     def is_anchor(self, layer: int) -> bool:
         if layer == 0:
@@ -68,7 +73,7 @@ class Workload:
 
 
 def preset(name: str, **kw) -> Workload:
-    """Named workloads: tiny, drift, scale, gqa, longctx."""
+    """Named workloads: tiny, drift, scale, gqa, longctx, ablation, stride."""
     if name == "tiny":
         w = Workload("tiny", 1, 1, 4, 0, 128, 64, "f32", 8, 4, 4, 16, 0.3)
     elif name == "drift":
@@ -80,6 +85,16 @@ def preset(name: str, **kw) -> Workload:
     elif name == "longctx":
         w = Workload("longctx", 32, 32, 32, 8, 4096, 128, "bf16", 64, 32, 32, 64, 0.6,
                      causal=True, near_ties=True)
+    elif name == "ablation":
+        # the sentinel-ablation shape (Sec. 5.2, Table 3): 256 query rows, 256
+        # key chunks, d = 64, top-12, 24 layers with one anchor; sentinel
+        # widths vary per study point
+        w = Workload("ablation", 1, 1, 24, 0, 256, 64, "f32", 12, 12, 12, 16, 0.05)
+    elif name == "stride":
+        # the cross-layer drift shape (Sec. 5.1, Table 2): 384 query rows, 192
+        # key chunks, top-12 with 24 near-miss and 12 random sentinels, 32
+        # layers with one anchor
+        w = Workload("stride", 1, 1, 32, 0, 384, 64, "f32", 12, 24, 12, 16, 0.2, n_keys=192)
     else:
         raise KeyError(name)
     return w.with_(**kw) if kw else w
@@ -112,10 +127,11 @@ class Generator:
         d = w.d
         rng = np.random.default_rng(w.seed)
         mu = rng.standard_normal((w.n_kv_heads, w.clusters, d))
-        zk = rng.integers(0, w.clusters, size=(w.n_kv_heads, w.n))
+        nk = w.nk
+        zk = rng.integers(0, w.clusters, size=(w.n_kv_heads, nk))
         zq = rng.integers(0, w.clusters, size=(w.n_heads, w.n))
         group = w.n_heads // w.n_kv_heads
-        K = np.empty((w.n_kv_heads, w.n, d), dtype=np.float64)
+        K = np.empty((w.n_kv_heads, nk, d), dtype=np.float64)
         for g in range(w.n_kv_heads):
             K[g] = mu[g][zk[g]]
         K += 0.3 * rng.standard_normal(K.shape)
@@ -128,10 +144,10 @@ class Generator:
         dups = None
         if w.near_ties:
             dups = []
-            n_dup = w.n // 4
+            n_dup = nk // 4
             for g in range(w.n_kv_heads):
-                dup = np.sort(rng.permutation(w.n)[:n_dup])
-                is_dup = np.zeros(w.n, dtype=bool)
+                dup = np.sort(rng.permutation(nk)[:n_dup])
+                is_dup = np.zeros(nk, dtype=bool)
                 is_dup[dup] = True
                 src = np.empty(n_dup, dtype=np.int64)
                 for t, j in enumerate(dup):

@@ -33,7 +33,7 @@ TOL = {"f32": 1e-5, "bf16": 2e-3}
 
 
 def problem_of(w, **kw) -> oracle.Problem:
-    p = oracle.Problem(w.n_heads, w.n_kv_heads, w.n, w.n, w.d, w.k, w.m, w.r, w.causal, w.gamma, w.seed)
+    p = oracle.Problem(w.n_heads, w.n_kv_heads, w.n, w.nk, w.d, w.k, w.m, w.r, w.causal, w.gamma, w.seed)
     return dataclasses.replace(p, **kw) if kw else p
 
 

@@ -238,6 +238,11 @@ ROLLOUTS = [
     # units), with a ragged last tile in the causal case
     ("scale", {"n_heads": 64, "n_kv_heads": 64, "n": 256, "n_layers": 4, "anchor_every": 2}),
     ("gqa", {"n_heads": 64, "n_kv_heads": 16, "n": 160, "n_layers": 4, "anchor_every": 2}),
+    # the fidelity studies' shapes: sentinel ablation with no near-miss
+    # slots and with no random slots; 384 query rows against 192 key chunks
+    ("ablation", {"m": 0, "r": 12, "rho": 0.05, "n_layers": 8}),
+    ("ablation", {"m": 24, "r": 0, "rho": 0.05, "n_layers": 8}),
+    ("stride", {"rho": 0.2, "n_layers": 8}),
 ]
 
 
