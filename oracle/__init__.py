@@ -16,7 +16,7 @@ from __future__ import annotations
 import ctypes
 import os
 import subprocess
-from dataclasses import dataclass
+from dataclasses import dataclass, field
 
 import numpy as np
 
@@ -43,6 +43,9 @@ class _Problem(ctypes.Structure):
         ("k", ctypes.c_int32), ("m", ctypes.c_int32), ("r", ctypes.c_int32),
         ("causal", ctypes.c_int32), ("pad_", ctypes.c_int32),
         ("gamma", ctypes.c_double), ("seed", ctypes.c_uint64),
+        ("n_sink", ctypes.c_int32), ("n_recent", ctypes.c_int32),
+        ("min_reuse", ctypes.c_int32), ("pad2_", ctypes.c_int32),
+        ("gamma_rows", ctypes.c_void_p),
     ]
 
 
@@ -60,18 +63,34 @@ class Problem:
     causal: bool = False
     gamma: float = 0.0
     seed: int = 0
+    n_sink: int = 0        # mandatory sentinels: the first n_sink chunks ...
+    n_recent: int = 0      # ... and the n_recent most recent valid chunks (Sec. 3.1, item 3)
+    min_reuse: int = 0     # hysteresis: rows (re)built at layer b keep their route through b + min_reuse
+    gamma_rows: object = field(default=None, compare=False)  # per-row guard margins (binary64 [rows]) or None
 
     @property
     def rows(self) -> int:
         return self.n_heads * self.n_q
 
+    @property
+    def sent_width(self) -> int:
+        """Sentinel slots per row: near-miss, random, then mandatory."""
+        return self.m + self.r + self.n_sink + self.n_recent
+
     def n_valid(self, i: int) -> int:
         return min(i + 1, self.n_k) if self.causal else self.n_k
 
     def _c(self) -> _Problem:
+        g = None
+        if self.gamma_rows is not None:
+            g = np.ascontiguousarray(self.gamma_rows, dtype=np.float64)
+            if g.shape != (self.rows,):
+                raise ValueError("gamma_rows must have one entry per row")
+            object.__setattr__(self, "_keep", g)  # (kept alive while the struct is in use)
         return _Problem(self.n_heads, self.n_kv_heads, self.n_q, self.n_k, self.d, self.k,
                         self.m, self.r, int(self.causal), 0, float(self.gamma),
-                        int(self.seed) & 0xFFFFFFFFFFFFFFFF)
+                        int(self.seed) & 0xFFFFFFFFFFFFFFFF, int(self.n_sink), int(self.n_recent),
+                        int(self.min_reuse), 0, None if g is None else g.ctypes.data)
 
 
 _lib = None
@@ -190,7 +209,7 @@ def new_ledger(p: Problem):
     """An empty ledger in the layout of Sec. 4.1: routes, sentinels, build layer, age."""
     return {
         "routes": np.full((p.rows, p.k), -1, dtype=np.int32),
-        "sent": np.full((p.rows, p.m + p.r), -1, dtype=np.int32),
+        "sent": np.full((p.rows, p.sent_width), -1, dtype=np.int32),
         "build": np.full(p.rows, -1, dtype=np.int32),
         "age": np.zeros(p.rows, dtype=np.int32),
     }

@@ -47,6 +47,18 @@
  *     (remaining pool size).  Both are uniform draws without replacement
  *     (Eq. (10)); rank sampling spares the small pools of early causal rows
  *     their long rejection runs;
+ *   - mandatory sentinels (Sec. 3.1, item 3): the sink chunks j < n_sink
+ *     and the recent chunks, the n_recent valid chunks at and below the
+ *     row's own position (position i when n_q == n_k, else the last key
+ *     chunk), minus any already in R or N, stored ascending after the random
+ *     slots (n_sink + n_recent slots, -1 padded); the random pool leaves
+ *     them out as well;
+ *   - per-row guard margins (Eq. (8), gamma_i >= 0): gamma_rows[row] when
+ *     given, else the scalar gamma;
+ *   - hysteresis (Sec. 3.2): a minimum reuse horizon of min_reuse layers --
+ *     a row (re)built at layer b is not rerouted at layers b+1 .. b+min_reuse
+ *     (0: off); the paper's optional larger margin after a refresh is left to
+ *     gamma_rows, which the caller may raise for such rows;
  *   - random sentinels persist until the row is next rebuilt;
  *   - score pairs: a (re)built row counts its n_i scores, a relay row counts
  *     |A| (valid candidate slots) plus n_i when it is rerouted;
@@ -70,6 +82,11 @@ typedef struct {
     int32_t pad_;
     double gamma;       /* guard margin of the trigger */
     uint64_t seed;      /* random-probe seed */
+    int32_t n_sink;     /* mandatory sentinels: the first n_sink chunks ... */
+    int32_t n_recent;   /* ... and the n_recent most recent valid chunks */
+    int32_t min_reuse;  /* a row (re)built at layer b keeps its route at layers b+1 .. b+min_reuse */
+    int32_t pad2_;
+    const double *gamma_rows; /* per-row guard margins gamma_i (NULL: gamma for every row) */
 } orc_problem;
 
 typedef struct {
@@ -197,17 +214,39 @@ static void split_route(const orc_scored *work, int ni, int kk, int mm, int32_t 
 
 /* ------------------------------------------------------- random sentinels */
 
-/* r probes drawn without replacement from the pool V_i minus (R u N).
- * excl is caller scratch of n_k bytes. */
+/* Mandatory sentinels of row i (Sec. 3.1, item 3): the sink chunks
+ * [0, n_sink) and the recent chunks [p - n_recent + 1, p], p the row's
+ * position (i when n_q == n_k, else n_k - 1), both cut to the valid chunks,
+ * without those already in R u N (marked in excl); written ascending to
+ * out[0 .. n_sink + n_recent), -1 padded, and marked in excl.  Returns how
+ * many were written. */
+static int build_mandatory(const orc_problem *P, int i, int ni, unsigned char *excl, int32_t *out)
+{
+    int width = P->n_sink + P->n_recent, w = 0;
+    int p = (P->n_q == P->n_k) ? i : P->n_k - 1;
+    if (p > ni - 1) p = ni - 1;
+    int lo = p - P->n_recent + 1;
+    if (lo < 0) lo = 0;
+    for (int j = 0; j < ni && w < width; ++j) {
+        int sink = j < P->n_sink, recent = P->n_recent > 0 && j >= lo && j <= p;
+        if ((sink || recent) && !excl[j]) {
+            out[w++] = j;
+            excl[j] = 1;
+        }
+    }
+    for (int t = w; t < width; ++t) out[t] = -1;
+    return w;
+}
+
+/* r probes drawn without replacement from the pool V_i minus (R u N u M).
+ * excl is caller scratch of n_k bytes marking R, N and M; nM is |M|. */
 static void draw_random(const orc_problem *P, int32_t layer, int64_t row, int ni,
-                        const int32_t *R, int nR, const int32_t *N, int nN, int32_t *out,
+                        int nR, int nN, int nM, int32_t *out, const unsigned char *excl_in,
                         unsigned char *excl)
 {
     int r = P->r;
-    memset(excl, 0, (size_t)P->n_k);
-    for (int t = 0; t < nR; ++t) excl[R[t]] = 1;
-    for (int t = 0; t < nN; ++t) excl[N[t]] = 1;
-    int pool = ni - nR - nN;
+    if (excl != excl_in) memcpy(excl, excl_in, (size_t)P->n_k);
+    int pool = ni - nR - nN - nM;
     if (pool <= r) {
         int w = 0;
         for (int j = 0; j < ni; ++j)
@@ -260,7 +299,10 @@ int orc_random_sentinels(const orc_problem *P, int32_t layer, int64_t row, int32
 {
     unsigned char *excl = (unsigned char *)malloc((size_t)P->n_k);
     if (!excl) return -2;
-    draw_random(P, layer, row, ni, R, nR, N, nN, out, excl);
+    memset(excl, 0, (size_t)P->n_k);
+    for (int t = 0; t < nR; ++t) excl[R[t]] = 1;
+    for (int t = 0; t < nN; ++t) excl[N[t]] = 1;
+    draw_random(P, layer, row, ni, nR, nN, 0, out, excl, excl);
     free(excl);
     return 0;
 }
@@ -333,18 +375,25 @@ int orc_route_bounds(const orc_problem *P, const float *Q, const float *K, const
 
 /* ---------------------------------------------------------------- anchor */
 
+static int sent_width(const orc_problem *P) { return P->m + P->r + P->n_sink + P->n_recent; }
+
 static void rebuild_row(const orc_problem *P, int32_t layer, const float *Q, const float *K,
                         int64_t row, orc_scored *work, unsigned char *excl, int32_t *routes,
                         int32_t *sent, int32_t *build, int32_t *age, int *ni_out)
 {
     int h = (int)(row / P->n_q), i = (int)(row % P->n_q);
-    int c = P->m + P->r;
+    int c = sent_width(P);
     int ni = rank_row(P, Q, K, h, i, work);
     int nR, nN;
     int32_t *R = routes + row * P->k;
     int32_t *C = sent + row * c;
     split_route(work, ni, P->k, P->m, R, &nR, C, &nN, NULL);
-    draw_random(P, layer, row, ni, R, nR, C, nN, C + P->m, excl);
+    /* C = near-miss slots, random slots, then mandatory slots */
+    memset(excl, 0, (size_t)P->n_k);
+    for (int t = 0; t < nR; ++t) excl[R[t]] = 1;
+    for (int t = 0; t < nN; ++t) excl[C[t]] = 1;
+    int nM = build_mandatory(P, i, ni, excl, C + P->m + P->r);
+    draw_random(P, layer, row, ni, nR, nN, nM, C + P->m, excl, excl);
     build[row] = layer;
     age[row] = 0;
     *ni_out = ni;
@@ -387,7 +436,7 @@ int orc_relay(const orc_problem *P, int32_t layer, const float *Q, const float *
     orc_scored *work = (orc_scored *)malloc(sizeof(orc_scored) * (size_t)P->n_k);
     unsigned char *excl = (unsigned char *)malloc((size_t)P->n_k);
     if (!work || !excl) { free(work); free(excl); return -2; }
-    int c = P->m + P->r;
+    int c = sent_width(P);
     int64_t total = 0;
     FOR_ROWS(P, rows, n_rows, idx, row) {
         int h = (int)(row / P->n_q);
@@ -412,7 +461,9 @@ int orc_relay(const orc_problem *P, int32_t layer, const float *Q, const float *
             if (s > b) { b = s; b_abs = absdot64(q, kr, P->d); }
         }
         int64_t own = n_cand;
-        int reroute = (n_sent > 0) && (b + P->gamma >= a);
+        double g = P->gamma_rows ? P->gamma_rows[row] : P->gamma;
+        int settled = P->min_reuse > 0 && layer - build[row] <= P->min_reuse;
+        int reroute = (n_sent > 0) && !settled && (b + g >= a);
         if (alpha) alpha[row] = a;
         if (beta) beta[row] = b;
         if (alpha_abs) alpha_abs[row] = a_abs;

@@ -13,6 +13,8 @@ typedef struct {
     int32_t n_heads, n_kv_heads, n_q, n_k, d, k, m, r, causal, pad_;
     double gamma;
     uint64_t seed;
+    int32_t n_sink, n_recent, min_reuse, pad2_;
+    const double *gamma_rows;
 } orc_problem;
 
 uint64_t orc_splitmix64(uint64_t z);
@@ -38,14 +40,19 @@ static float draw(int integer)
     return (float)((double)(state >> 11) / 9007199254740992.0 - 0.5);
 }
 
-static int run(int H, int Hkv, int n, int d, int k, int m, int r, int causal, int integer, double gamma)
+static int run(int H, int Hkv, int n, int d, int k, int m, int r, int causal, int integer, double gamma,
+               int n_sink, int n_recent, int min_reuse, int per_row_gamma)
 {
-    orc_problem P = {H, Hkv, n, n, d, k, m, r, causal, 0, gamma, 7};
     const int64_t rows = (int64_t)H * n;
+    double *gr = malloc(sizeof(double) * (size_t)rows);
+    for (int64_t t = 0; t < rows; ++t) gr[t] = (t % 3 == 0) ? INFINITY : (t % 3 == 1 ? 0.0 : 0.01);
+    orc_problem P = {H, Hkv, n, n, d, k, m, r, causal, 0, gamma, 7, n_sink, n_recent, min_reuse, 0,
+                     per_row_gamma ? gr : NULL};
+    const int c = m + r + n_sink + n_recent;
     float *Q = malloc(sizeof(float) * (size_t)(rows * d));
     float *K = malloc(sizeof(float) * (size_t)((int64_t)Hkv * n * d));
     int32_t *routes = malloc(sizeof(int32_t) * (size_t)(rows * k));
-    int32_t *sent = malloc(sizeof(int32_t) * (size_t)(rows * (m + r) + 1));
+    int32_t *sent = malloc(sizeof(int32_t) * (size_t)(rows * c + 1));
     int32_t *build = malloc(sizeof(int32_t) * (size_t)rows), *age = malloc(sizeof(int32_t) * (size_t)rows);
     uint8_t *mask = malloc((size_t)rows);
     double *rs = malloc(sizeof(double) * (size_t)(rows * k)), *bounds = malloc(sizeof(double) * (size_t)(rows * 8));
@@ -73,19 +80,21 @@ static int run(int H, int Hkv, int n, int d, int k, int m, int r, int causal, in
         P.r = r;
     }
     free(Q); free(K); free(routes); free(sent); free(build); free(age); free(mask); free(rs); free(bounds);
-    free(al); free(be); free(aa); free(ba); free(rp);
+    free(al); free(be); free(aa); free(ba); free(rp); free(gr);
     return bad;
 }
 
 int main(void)
 {
     int bad = 0;
-    bad |= run(1, 1, 40, 16, 5, 3, 4, 0, 0, 0.0);
-    bad |= run(2, 1, 33, 8, 4, 2, 6, 1, 0, 0.0);      /* causal GQA, early rows with n_i < k */
-    bad |= run(2, 2, 20, 8, 20, 0, 0, 0, 0, 0.0);     /* k = n_k, no sentinels */
-    bad |= run(1, 1, 30, 8, 6, 6, 20, 0, 1, 0.0);     /* exact ties; pools below r */
-    bad |= run(1, 1, 64, 8, 8, 4, 16, 1, 1, INFINITY); /* every row rerouted */
-    bad |= run(1, 1, 64, 8, 8, 4, 16, 0, 0, -INFINITY);
+    bad |= run(1, 1, 40, 16, 5, 3, 4, 0, 0, 0.0, 0, 0, 0, 0);
+    bad |= run(2, 1, 33, 8, 4, 2, 6, 1, 0, 0.0, 0, 0, 0, 0);      /* causal GQA, early rows with n_i < k */
+    bad |= run(2, 2, 20, 8, 20, 0, 0, 0, 0, 0.0, 0, 0, 0, 0);     /* k = n_k, no sentinels */
+    bad |= run(1, 1, 30, 8, 6, 6, 20, 0, 1, 0.0, 0, 0, 0, 0);     /* exact ties; pools below r */
+    bad |= run(1, 1, 64, 8, 8, 4, 16, 1, 1, INFINITY, 0, 0, 0, 0); /* every row rerouted */
+    bad |= run(1, 1, 64, 8, 8, 4, 16, 0, 0, -INFINITY, 0, 0, 0, 0);
+    bad |= run(2, 1, 40, 8, 4, 3, 5, 1, 0, 0.0, 2, 3, 1, 1);      /* mandatory sentinels, hysteresis, per-row gamma */
+    bad |= run(1, 1, 24, 8, 6, 4, 8, 0, 1, 0.0, 4, 4, 0, 1);      /* mandatory slots crowding a small pool */
     if (bad) { fprintf(stderr, "oracle call failed\n"); return 1; }
     printf("oracle driver ok\n");
     return 0;
