@@ -56,7 +56,8 @@ typedef enum {
 typedef enum { RR_F32 = 0, RR_BF16 = 1 } rr_dtype;
 
 /* Shape and rule parameters.  Supported: d in {32, 64, 128} (and 256 for
- * bf16); 1 <= k <= n_k; k + m <= 128; k + m + r <= 256; n_k <= 8192;
+ * bf16); 1 <= k <= n_k; k + m <= 128; k + m + r + n_sink + n_recent <= 256;
+ * n_k <= 8192;
  * n_heads a multiple of n_kv_heads; gamma not NaN.  gamma is the guard
  * margin of Eq. (8); the paper uses gamma >= 0 (0 by default, Table 1);
  * +INFINITY refreshes every row that has a sentinel and -INFINITY refreshes
@@ -92,14 +93,31 @@ typedef struct {
     float gamma;        /* guard margin */
     uint32_t options;   /* rr_option bits (0: defaults) */
     uint64_t seed;
+    /* Mandatory sentinels (Sec. 3.1, item 3): the sink chunks j < n_sink and
+     * the recent chunks -- the n_recent valid chunks up to the row's position
+     * (row i when n_q == n_k, else the last key chunk) -- that are not in R or
+     * N, kept ascending in n_sink + n_recent extra sentinel slots after the
+     * random ones (-1 padded) and left out of the random draws. */
+    int32_t n_sink;
+    int32_t n_recent;
+    /* Minimum reuse horizon (Sec. 3.2, Hysteresis): a row (re)built at layer
+     * b is not rerouted at layers b+1 .. b+min_reuse.  0: off. */
+    int32_t min_reuse;
+    int32_t reserved;           /* must be 0 */
+    /* Per-row guard margins gamma_i of Eq. (8): a device array of H_q*n_q
+     * binary32 values read by every relay (the caller may change them between
+     * layers, e.g. to raise the margin of recently refreshed rows); NULL: the
+     * scalar gamma for every row.  Values must not be NaN. */
+    const float *gamma_rows;
 } rr_config;
 
 typedef struct rr_ledger rr_ledger;
 
 /* Route ledger (Sec. 3.1, Eq. (4); state tensors of Sec. 4.1).  Allocates,
  * on the current HIP device, the structure-of-arrays ledger -- routes
- * [H_q*n_q, k], sentinels [H_q*n_q, m+r] (near-miss slots first, sorted by
- * id; then random slots in draw order; -1 padded), build layer and age
+ * [H_q*n_q, k], sentinels [H_q*n_q, m+r+n_sink+n_recent] (near-miss slots
+ * first, sorted by id; then random slots in draw order; then mandatory slots,
+ * sorted by id; -1 padded), build layer and age
  * [H_q*n_q] int32 -- plus the per-row scratch of the relay path.  *out
  * receives the handle (NULL on failure).  Returns RR_ERR_INVALID /
  * RR_ERR_UNSUPPORTED for a bad config, RR_ERR_OOM if allocation fails. */
@@ -151,8 +169,9 @@ rr_status rr_relay_layer(rr_ledger *ledger, int32_t layer, const void *Qc, const
  * device memory at call time: code under HIP graph capture, tight serving
  * loops, harnesses that forbid hipMalloc.  The same computation and kernels as
  * rr_relay_layer, on a ledger the caller owns, in the layout rr_ledger_export
- * writes: led_routes [H_q*n_q, k], led_sent [H_q*n_q, m+r] (may be NULL when
- * m + r = 0), led_build and led_age [H_q*n_q] int32, all device memory,
+ * writes: led_routes [H_q*n_q, k], led_sent [H_q*n_q, m+r+n_sink+n_recent]
+ * (may be NULL when that width is 0), led_build and led_age [H_q*n_q]
+ * int32, all device memory,
  * updated in place.  The relay's scratch (flags, alpha / beta, per-workgroup
  * partials, call totals, threshold seeds, a completion counter) lives in a
  * static device area of the library, 4 MiB per GPU, held until the process
@@ -181,7 +200,8 @@ rr_status rr_full_route(const rr_config *cfg, const void *Qc, const void *Kc, in
 const int32_t *rr_ledger_routes(const rr_ledger *ledger);
 
 /* Copies the ledger state into caller device buffers (each may be NULL):
- * routes [rows,k], sent [rows,m+r], build [rows], age [rows] int32. */
+ * routes [rows,k], sent [rows,m+r+n_sink+n_recent], build [rows], age [rows]
+ * int32. */
 rr_status rr_ledger_export(const rr_ledger *ledger, int32_t *routes, int32_t *sent,
                            int32_t *build, int32_t *age, void *hip_stream);
 
@@ -237,7 +257,7 @@ rr_status rr_unconverged_rows(uint64_t *count);
 rr_status rr_set_sweep_cap(int32_t cap);
 
 /* Number of bytes of ledger index storage (routes plus sentinels) for a
- * config: H_q * n_q * (k + m + r) * 4. */
+ * config: H_q * n_q * (k + m + r + n_sink + n_recent) * 4. */
 size_t rr_ledger_index_bytes(const rr_config *cfg);
 
 const char *rr_status_string(rr_status status);

@@ -110,6 +110,9 @@ rr_status hip_fail(hipError_t e, const char *what)
 
 int64_t rows_of(const rr_config &c) { return (int64_t)c.n_heads * c.n_q; }
 
+// Sentinel slots per ledger row: near-miss, random, then mandatory.
+int sent_width(const rr_config &c) { return c.m + c.r + c.n_sink + c.n_recent; }
+
 // Sum of n_i over all rows: the score pairs of one full routing pass.
 int64_t full_pairs(const rr_config &c)
 {
@@ -140,13 +143,16 @@ rr_status validate(const rr_config *c, bool ledger)
     if (c->d < 1) return fail(RR_ERR_INVALID, "d must be >= 1");
     if (c->k < 1 || c->k > c->n_k) return fail(RR_ERR_INVALID, "k must lie in [1, n_k]");
     if (c->m < 0 || c->r < 0) return fail(RR_ERR_INVALID, "m and r must be >= 0");
+    if (c->n_sink < 0 || c->n_recent < 0 || c->min_reuse < 0)
+        return fail(RR_ERR_INVALID, "n_sink, n_recent and min_reuse must be >= 0");
+    if (c->reserved != 0) return fail(RR_ERR_INVALID, "rr_config.reserved must be 0");
     uint32_t gbits;
     std::memcpy(&gbits, &c->gamma, sizeof(gbits));
     if ((gbits & 0x7FFFFFFFu) > 0x7F800000u) return fail(RR_ERR_INVALID, "gamma is NaN");  // (bit test: device passes assume no NaN)
-    const int m = ledger ? c->m : 0, r = ledger ? c->r : 0;
+    const int m = ledger ? c->m : 0, r = ledger ? c->r + c->n_sink + c->n_recent : 0;
     if (!rr::route_supported(c->dtype, c->d, c->k + m))
         return fail(RR_ERR_UNSUPPORTED, "unsupported (dtype, d, k+m): d in {32,64,128} (256 for bf16), k+m <= 128");
-    if (c->k + m + r > 256) return fail(RR_ERR_UNSUPPORTED, "k + m + r must be <= 256");
+    if (c->k + m + r > 256) return fail(RR_ERR_UNSUPPORTED, "k + m + r + n_sink + n_recent must be <= 256");
     if (c->n_k > 8192) return fail(RR_ERR_UNSUPPORTED, "n_k must be <= 8192");
     if (c->n_heads > 1024) return fail(RR_ERR_UNSUPPORTED, "n_heads must be <= 1024");
     if (rows_of(*c) * (int64_t)(c->k + m + r + 1) >= (int64_t)INT32_MAX || rows_of(*c) * c->d >= (int64_t)INT32_MAX * 8)
@@ -278,6 +284,10 @@ rr::RouteArgs route_args(const rr_config &c, const void *Q, const void *K)
     a.k = c.k;
     a.m = c.m;
     a.r = c.r;
+    a.n_sink = c.n_sink;
+    a.n_recent = c.n_recent;
+    a.min_reuse = c.min_reuse;
+    a.gamma_rows = c.gamma_rows;
     a.causal = c.causal;
     a.tile_rows = rr::route_tile_rows(c.k + c.m, c.n_heads, c.n_q);
     a.tiles_per_head = (c.n_q + a.tile_rows - 1) / a.tile_rows;
@@ -413,6 +423,9 @@ rr_status relay_launch(const rr_config &c, const RelayBuffers &b, int32_t layer,
         s.k = c.k;
         s.m = c.m;
         s.r = c.r;
+        s.n_mand = c.n_sink + c.n_recent;
+        s.min_reuse = c.min_reuse;
+        s.gamma_rows = c.gamma_rows;
         s.causal = c.causal;
         s.layer = layer;
         rr::RescoreGeometry geo;
@@ -492,7 +505,7 @@ const char *rr_last_error(void) { return g_err.c_str(); }
 size_t rr_ledger_index_bytes(const rr_config *c)
 {
     if (!c) return 0;
-    return (size_t)rows_of(*c) * (size_t)(c->k + c->m + c->r) * sizeof(int32_t);
+    return (size_t)rows_of(*c) * (size_t)(c->k + sent_width(*c)) * sizeof(int32_t);
 }
 
 rr_status rr_ledger_create(const rr_config *cfg, rr_ledger **out)
@@ -515,7 +528,7 @@ rr_status rr_ledger_create(const rr_config *cfg, rr_ledger **out)
     // per-workgroup partial slots of a relay layer
     const int64_t max_blocks = relay_partial_slots(*cfg);
     if ((st = alloc(&L->routes, rows * cfg->k, "routes")) != RR_OK ||
-        (st = alloc(&L->sent, rows * (cfg->m + cfg->r), "sentinels")) != RR_OK ||
+        (st = alloc(&L->sent, rows * sent_width(*cfg), "sentinels")) != RR_OK ||
         (st = alloc(&L->build, rows, "build")) != RR_OK || (st = alloc(&L->age, rows, "age")) != RR_OK ||
         (st = alloc(&L->stat_nrr, 1, "stat_nrr")) != RR_OK ||
         (st = alloc(&L->flags, rows, "flags")) != RR_OK || (st = alloc(&L->alpha, rows, "alpha")) != RR_OK ||
@@ -542,7 +555,7 @@ rr_status rr_ledger_create(const rr_config *cfg, rr_ledger **out)
     // One-time initialisation (outside any hot path): an empty ledger.
     hipError_t e = hipSuccess;
     if (e == hipSuccess) e = hipMemset(L->routes, 0xFF, sizeof(int32_t) * rows * cfg->k);
-    if (e == hipSuccess && cfg->m + cfg->r > 0) e = hipMemset(L->sent, 0xFF, sizeof(int32_t) * rows * (cfg->m + cfg->r));
+    if (e == hipSuccess && sent_width(*cfg) > 0) e = hipMemset(L->sent, 0xFF, sizeof(int32_t) * rows * sent_width(*cfg));
     if (e == hipSuccess) e = hipMemset(L->build, 0xFF, sizeof(int32_t) * rows);
     if (e == hipSuccess) e = hipMemset(L->age, 0, sizeof(int32_t) * rows);
     if (e == hipSuccess && L->done) e = hipMemset(L->done, 0, sizeof(uint32_t));
@@ -641,7 +654,7 @@ rr_status rr_relay_layer_static(const rr_config *cfg, int32_t layer, const void 
     rr_status st = validate(cfg, true);
     if (st != RR_OK) return st;
     const rr_config &c = *cfg;
-    if (!Qc || !Kc || !led_routes || !led_build || !led_age || (!led_sent && c.m + c.r > 0))
+    if (!Qc || !Kc || !led_routes || !led_build || !led_age || (!led_sent && sent_width(c) > 0))
         return fail(RR_ERR_INVALID, "Qc, Kc and the ledger arrays (routes, sent, build, age) are required");
     if (layer < 0) return fail(RR_ERR_INVALID, "layer must be >= 0");
     RelayPlan plan = relay_plan(c);
@@ -695,6 +708,8 @@ rr_status rr_full_route(const rr_config *cfg, const void *Qc, const void *Kc, in
     rr_config c = *cfg;
     c.m = 0;
     c.r = 0;
+    c.n_sink = 0;
+    c.n_recent = 0;
     rr::RouteArgs a = route_args(c, Qc, Kc);
     a.unconverged = ds->unconverged;
     a.mode = rr::MODE_FULL;
@@ -720,8 +735,8 @@ rr_status rr_ledger_export(const rr_ledger *L, int32_t *routes, int32_t *sent, i
     const rr_config &c = L->cfg;
     hipError_t e = hipSuccess;
     if (routes) e = hipMemcpyAsync(routes, L->routes, sizeof(int32_t) * L->rows * c.k, hipMemcpyDeviceToDevice, s);
-    if (e == hipSuccess && sent && c.m + c.r > 0)
-        e = hipMemcpyAsync(sent, L->sent, sizeof(int32_t) * L->rows * (c.m + c.r), hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess && sent && sent_width(c) > 0)
+        e = hipMemcpyAsync(sent, L->sent, sizeof(int32_t) * L->rows * sent_width(c), hipMemcpyDeviceToDevice, s);
     if (e == hipSuccess && build) e = hipMemcpyAsync(build, L->build, sizeof(int32_t) * L->rows, hipMemcpyDeviceToDevice, s);
     if (e == hipSuccess && age) e = hipMemcpyAsync(age, L->age, sizeof(int32_t) * L->rows, hipMemcpyDeviceToDevice, s);
     return e == hipSuccess ? RR_OK : hip_fail(e, "ledger export");
@@ -732,14 +747,14 @@ rr_status rr_ledger_import(rr_ledger *L, int32_t layer, const int32_t *routes, c
 {
     if (!L) return fail(RR_ERR_INVALID, "ledger is NULL");
     const rr_config &c = L->cfg;
-    if (!routes || !build || !age || (!sent && c.m + c.r > 0))
+    if (!routes || !build || !age || (!sent && sent_width(c) > 0))
         return fail(RR_ERR_INVALID, "routes, sent, build and age are required");
     if (layer < 0) return fail(RR_ERR_INVALID, "layer must be >= 0");
     DeviceGuard g(L->device);
     hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
     hipError_t e = hipMemcpyAsync(L->routes, routes, sizeof(int32_t) * L->rows * c.k, hipMemcpyDeviceToDevice, s);
-    if (e == hipSuccess && c.m + c.r > 0)
-        e = hipMemcpyAsync(L->sent, sent, sizeof(int32_t) * L->rows * (c.m + c.r), hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess && sent_width(c) > 0)
+        e = hipMemcpyAsync(L->sent, sent, sizeof(int32_t) * L->rows * sent_width(c), hipMemcpyDeviceToDevice, s);
     if (e == hipSuccess) e = hipMemcpyAsync(L->build, build, sizeof(int32_t) * L->rows, hipMemcpyDeviceToDevice, s);
     if (e == hipSuccess) e = hipMemcpyAsync(L->age, age, sizeof(int32_t) * L->rows, hipMemcpyDeviceToDevice, s);
     if (e != hipSuccess) return hip_fail(e, "ledger import");

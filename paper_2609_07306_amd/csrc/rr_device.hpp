@@ -68,6 +68,22 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int mask)
 
 __device__ __forceinline__ uint32_t lanemask_lt32(int l32) { return (1u << l32) - 1u; }
 
+// ------------------------------------------------------------ trigger
+//
+// Eq. (8): a row keeps its route while alpha > beta + gamma_i.  It is
+// rerouted when it has a sentinel, its minimum reuse horizon has passed
+// (Sec. 3.2, Hysteresis: a row (re)built at layer b keeps its route at
+// layers b+1 .. b+min_reuse; 0 disables it) and beta + gamma_i >= alpha.
+// gamma_i is gamma_rows[row] when the caller gives per-row margins.
+__device__ __forceinline__ bool relay_trigger(int n_sent, float alpha, float beta, float gamma,
+                                              const float *gamma_rows, int64_t row, int layer, int build,
+                                              int min_reuse)
+{
+    const float g = gamma_rows ? gamma_rows[row] : gamma;
+    const bool settled = min_reuse > 0 && layer - build <= min_reuse;
+    return n_sent > 0 && !settled && (beta + g >= alpha);
+}
+
 // ------------------------------------------------------------ probe hash
 //
 // splitmix64 output function (Steele, Lea and Flood, OOPSLA 2014): add the

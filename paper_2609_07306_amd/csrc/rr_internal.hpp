@@ -27,6 +27,9 @@ struct RouteArgs {
     const void *K;
     int32_t n_heads, n_kv_heads, n_q, n_k, d;
     int32_t k, m, r;  // the kernel selects T = k + m chunks per row
+    int32_t n_sink, n_recent;  // mandatory sentinels (sentinel slots: m near-miss, r random, n_sink + n_recent mandatory)
+    int32_t min_reuse;         // relay: minimum reuse horizon in layers (0: none)
+    const float *gamma_rows;   // relay: per-row guard margins, or null (gamma for every row)
     int32_t causal;
     int32_t layer;
     int32_t mode;

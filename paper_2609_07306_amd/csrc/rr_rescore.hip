@@ -120,7 +120,7 @@ __global__ __launch_bounds__(kThreads) void rescore_kernel(RescoreArgs a)
     const int i0 = blk * RB + w * rpw;  // this wave's rows: i0 .. i0 + rpw - 1
     const int nrows = max(0, min(rpw, a.n_q - i0));
     const int group = a.n_heads / a.n_kv_heads;
-    const int c_sent = a.m + a.r, c_led = a.k + c_sent;
+    const int c_sent = a.m + a.r + a.n_mand, c_led = a.k + c_sent;
     const int rounds = (c_led + CPR - 1) / CPR;
     const unsigned char *Kg = reinterpret_cast<const unsigned char *>(a.K) + (int64_t)(h / group) * a.n_k * ROWB;
     const unsigned char *Qb = reinterpret_cast<const unsigned char *>(a.Q);
@@ -207,7 +207,8 @@ __global__ __launch_bounds__(kThreads) void rescore_kernel(RescoreArgs a)
     if (lane < nrows) {
         const int i = i0 + lane;
         const int64_t row = row0 + lane;
-        const bool flag = my_ns > 0 && (my_b + a.gamma >= my_a);
+        const bool flag = relay_trigger(my_ns, my_a, my_b, a.gamma, a.gamma_rows, row, a.layer,
+                                        a.min_reuse > 0 ? a.led_build[row] : 0, a.min_reuse);
         a.flags[row] = flag ? 1 : 0;
         if (a.mask_out) a.mask_out[row] = flag ? 1 : 0;
         a.alpha[row] = my_a;
@@ -245,7 +246,7 @@ template <typename DT, int D>
 hipError_t launch_d(const RescoreArgs &a, hipStream_t stream)
 {
     const int grid = a.n_heads * a.blocks_per_head;
-    const int c = a.k + a.m + a.r;
+    const int c = a.k + a.m + a.r + a.n_mand;
     if (c <= 64)
         hipLaunchKernelGGL((rescore_kernel<DT, D, 1>), dim3(grid), dim3(kThreads), 0, stream, a);
     else if (c <= 128)

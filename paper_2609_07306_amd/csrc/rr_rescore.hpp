@@ -22,6 +22,9 @@ struct RescoreArgs {
     const void *K;
     int32_t n_heads, n_kv_heads, n_q, n_k, d;
     int32_t k, m, r;
+    int32_t n_mand;           // mandatory sentinel slots after the random ones
+    int32_t min_reuse;        // minimum reuse horizon in layers (0: none)
+    const float *gamma_rows;  // per-row guard margins, or null (gamma for every row)
     int32_t causal;
     int32_t layer;
     int32_t blocks_per_head;  // ceil(n_q / rows per block)

@@ -107,7 +107,7 @@ __global__ __launch_bounds__(128 * NW) void rescore_dense_kernel(RescoreArgs a)
     tile_of_block(blockIdx.x, a.n_heads, a.n_kv_heads, a.blocks_per_head, h, t);
     const int i0 = t * BM;
     const int64_t g0 = (int64_t)h * a.n_q + i0;  // first row of the tile
-    const int c_sent = a.m + a.r, c_led = a.k + c_sent;
+    const int c_sent = a.m + a.r + a.n_mand, c_led = a.k + c_sent;
 
     // the tile's longest valid key range (tiles always hold a row), and the
     // first two key stages, the query fragments and the ledger rows are all
@@ -243,7 +243,8 @@ __global__ __launch_bounds__(128 * NW) void rescore_dense_kernel(RescoreArgs a)
         const float al = fminf(s_amin[0][tid], s_amin[1][tid]);
         const float be = fmaxf(s_bmax[0][tid], s_bmax[1][tid]);
         const int nc = s_nc[tid], ns = s_ns[tid];
-        const bool flag = ns > 0 && (be + a.gamma >= al);
+        const bool flag = relay_trigger(ns, al, be, a.gamma, a.gamma_rows, row, a.layer,
+                                        a.min_reuse > 0 ? a.led_build[row] : 0, a.min_reuse);
         a.flags[row] = flag ? 1 : 0;
         if (a.mask_out) a.mask_out[row] = flag ? 1 : 0;
         a.alpha[row] = al;

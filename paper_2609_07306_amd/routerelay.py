@@ -41,6 +41,8 @@ class _Config(ctypes.Structure):
         ("n_k", ctypes.c_int32), ("d", ctypes.c_int32), ("k", ctypes.c_int32), ("m", ctypes.c_int32),
         ("r", ctypes.c_int32), ("dtype", ctypes.c_int32), ("causal", ctypes.c_int32),
         ("gamma", ctypes.c_float), ("options", ctypes.c_uint32), ("seed", ctypes.c_uint64),
+        ("n_sink", ctypes.c_int32), ("n_recent", ctypes.c_int32), ("min_reuse", ctypes.c_int32),
+        ("reserved", ctypes.c_int32), ("gamma_rows", ctypes.c_void_p),
     ]
 
 
@@ -102,22 +104,37 @@ class Config:
     gamma: float = 0.0
     seed: int = 0
     relay: str = "auto"  # relay schedule: "auto" | "one_pass" | "split" (rr_option)
+    n_sink: int = 0      # mandatory sentinels: sink chunks ...
+    n_recent: int = 0    # ... and recent chunks
+    min_reuse: int = 0   # minimum reuse horizon (layers)
+    gamma_rows: object = None  # per-row guard margins: float32 device tensor [rows], or None
 
     @property
     def rows(self) -> int:
         return self.n_heads * self.n_q
 
+    @property
+    def sent_width(self) -> int:
+        return self.m + self.r + self.n_sink + self.n_recent
+
     def c(self) -> _Config:
+        g = None
+        if self.gamma_rows is not None:
+            t = self.gamma_rows
+            if t.dtype != torch.float32 or tuple(t.shape) != (self.rows,):
+                raise ValueError("gamma_rows must be a float32 tensor with one entry per row")
+            g = _ptr(t)
         return _Config(self.n_heads, self.n_kv_heads, self.n_q, self.n_k, self.d, self.k, self.m,
                        self.r, RR_BF16 if self.dtype == "bf16" else RR_F32, int(self.causal),
                        float(self.gamma), _RELAY_OPTIONS[self.relay],
-                       int(self.seed) & 0xFFFFFFFFFFFFFFFF)
+                       int(self.seed) & 0xFFFFFFFFFFFFFFFF, int(self.n_sink), int(self.n_recent),
+                       int(self.min_reuse), 0, g)
 
     @staticmethod
     def of(w) -> "Config":
         """From a synth.Workload."""
         return Config(w.n_heads, w.n_kv_heads, w.n, w.nk, w.d, w.k, w.m, w.r, w.dtype, w.causal,
-                      w.gamma, w.seed)
+                      w.gamma, w.seed, n_sink=w.n_sink, n_recent=w.n_recent, min_reuse=w.min_reuse)
 
 
 def _ptr(t):
@@ -198,7 +215,7 @@ def relay_static(cfg: Config, layer: int, Q, K, ledger, routes=None, mask=None, 
     c = cfg
     _check(lib.rr_relay_layer_static(
         ctypes.byref(cfg.c()), layer, q, k, _out(ledger["routes"], (c.rows, c.k), torch.int32),
-        _out(ledger["sent"], (c.rows, c.m + c.r), torch.int32) if c.m + c.r else None,
+        _out(ledger["sent"], (c.rows, c.sent_width), torch.int32) if c.sent_width else None,
         _out(ledger["build"], (c.rows,), torch.int32), _out(ledger["age"], (c.rows,), torch.int32),
         _out(routes, (c.rows, c.k), torch.int32), _out(mask, (c.rows,), torch.uint8),
         _out(pairs, (1,), torch.int64), _out(n_rerouted, (1,), torch.int32), _stream(stream)))
@@ -256,18 +273,18 @@ class Ledger:
         dev = torch.device("cuda", torch.cuda.current_device())
         out = {
             "routes": torch.empty((c.rows, c.k), dtype=torch.int32, device=dev),
-            "sent": torch.empty((c.rows, c.m + c.r), dtype=torch.int32, device=dev),
+            "sent": torch.empty((c.rows, c.sent_width), dtype=torch.int32, device=dev),
             "build": torch.empty((c.rows,), dtype=torch.int32, device=dev),
             "age": torch.empty((c.rows,), dtype=torch.int32, device=dev),
         }
-        _check(lib.rr_ledger_export(self._h, _ptr(out["routes"]), _ptr(out["sent"]) if c.m + c.r else None,
+        _check(lib.rr_ledger_export(self._h, _ptr(out["routes"]), _ptr(out["sent"]) if c.sent_width else None,
                                     _ptr(out["build"]), _ptr(out["age"]), _stream(stream)))
         return out
 
     def import_(self, layer: int, routes, sent, build, age, stream=None):
         c = self.cfg
         _check(lib.rr_ledger_import(self._h, layer, _out(routes, (c.rows, c.k), torch.int32),
-                                    _out(sent, (c.rows, c.m + c.r), torch.int32) if c.m + c.r else None,
+                                    _out(sent, (c.rows, c.sent_width), torch.int32) if c.sent_width else None,
                                     _out(build, (c.rows,), torch.int32), _out(age, (c.rows,), torch.int32),
                                     _stream(stream)))
 

@@ -53,6 +53,9 @@ class Workload:
     seed: int = 0
     gamma: float = 0.0
     n_keys: int = 0            # key chunks n_k when it differs from n_q = n (0: n_k = n)
+    n_sink: int = 0            # mandatory sink sentinels
+    n_recent: int = 0          # mandatory recent sentinels
+    min_reuse: int = 0         # minimum reuse horizon (layers)
     extra: dict = field(default_factory=dict, compare=False)
 
     @property

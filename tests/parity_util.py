@@ -33,7 +33,8 @@ TOL = {"f32": 1e-5, "bf16": 2e-3}
 
 
 def problem_of(w, **kw) -> oracle.Problem:
-    p = oracle.Problem(w.n_heads, w.n_kv_heads, w.n, w.nk, w.d, w.k, w.m, w.r, w.causal, w.gamma, w.seed)
+    p = oracle.Problem(w.n_heads, w.n_kv_heads, w.n, w.nk, w.d, w.k, w.m, w.r, w.causal, w.gamma, w.seed,
+                       n_sink=w.n_sink, n_recent=w.n_recent, min_reuse=w.min_reuse)
     return dataclasses.replace(p, **kw) if kw else p
 
 
@@ -58,10 +59,9 @@ def route_ties(p, Qf, Kf, rows=None):
 
 
 def trigger_ties(p, out):
-    if not np.isfinite(p.gamma):
-        return np.zeros(len(out["alpha"]), dtype=bool)
+    g = p.gamma_rows if p.gamma_rows is not None else np.full(len(out["alpha"]), p.gamma)
     with np.errstate(invalid="ignore"):
-        diff = np.abs(out["alpha"] - (out["beta"] + p.gamma))
+        diff = np.where(np.isfinite(g), np.abs(out["alpha"] - (out["beta"] + g)), np.inf)
         t = tau(out["alpha"], out["beta"], out["alpha_abs"], out["beta_abs"], p.d)
         tie = np.nan_to_num(diff, nan=np.inf) < t
     return tie
@@ -102,9 +102,10 @@ def n_valid_rows(p):
     return np.minimum(i + 1, p.n_k) if p.causal else np.full(p.rows, p.n_k)
 
 
-def rollout_compare(w, gamma=None, check_scores=True, relay="auto"):
+def rollout_compare(w, gamma=None, check_scores=True, relay="auto", gamma_rows=None):
     """Runs the workload's anchor/relay schedule on the GPU and on the oracle
-    (relay: the relay schedule, "auto", "one_pass" or "split").
+    (relay: the relay schedule, "auto", "one_pass" or "split"; gamma_rows:
+    per-row guard margins, binary32 values, or None).
 
     Returns a dict of statistics; raises AssertionError on any mismatch of a
     trusted row."""
@@ -112,6 +113,10 @@ def rollout_compare(w, gamma=None, check_scores=True, relay="auto"):
         w = w.with_(gamma=gamma)
     p = problem_of(w)
     cfg = dataclasses.replace(rr.Config.of(w), relay=relay)
+    if gamma_rows is not None:
+        g32 = np.ascontiguousarray(gamma_rows, dtype=np.float32)
+        p = dataclasses.replace(p, gamma_rows=g32.astype(np.float64))
+        cfg = dataclasses.replace(cfg, gamma_rows=torch.from_numpy(g32).to(torch.device("cuda", torch.cuda.current_device())))
     L = rr.Ledger(cfg)
     ref = oracle.new_ledger(p)
     trusted = np.zeros(p.rows, dtype=bool)

@@ -39,8 +39,10 @@ def test_library_exports_every_declared_symbol():
 
 def test_config_struct_layout():
     rr = _rr()
-    assert ctypes.sizeof(rr._Config) == 56
+    assert ctypes.sizeof(rr._Config) == 80
     assert rr._Config.seed.offset == 48 and rr._Config.gamma.offset == 40
+    assert rr._Config.n_sink.offset == 56 and rr._Config.reserved.offset == 68
+    assert rr._Config.gamma_rows.offset == 72
 
 
 def test_status_strings():
@@ -62,6 +64,8 @@ def _cfg(**kw):
     (dict(n_q=0), -1), (dict(causal=True, n_q=32), -1), (dict(gamma=math.nan), -1),
     (dict(d=48), -5), (dict(d=256), -5), (dict(k=60, m=70), -5), (dict(n_k=9000, n_q=9000), -5),
     (dict(k=64, m=64, r=200, n_k=4096), -5),
+    (dict(n_sink=-1), -1), (dict(n_recent=-2), -1), (dict(min_reuse=-1), -1),
+    (dict(k=32, m=32, r=160, n_sink=16, n_recent=17, n_k=4096, n_q=4096), -5),
 ])
 def test_invalid_configs_rejected_before_any_launch(kw, status):
     rr = _rr()
@@ -72,7 +76,7 @@ def test_invalid_configs_rejected_before_any_launch(kw, status):
     assert not h.value
     assert rr.lib.rr_last_error()
     # the stateless path validates the same way (m and r are ignored there)
-    if "m" not in kw and "r" not in kw:
+    if not set(kw) & {"m", "r", "n_sink", "n_recent", "min_reuse"}:
         fake = ctypes.c_void_p(0x1000)
         got = rr.lib.rr_full_route(ctypes.byref(cfg.c()), fake, fake, fake, None, None, None)
         assert got == status
@@ -122,6 +126,21 @@ def test_null_arguments():
     assert rr.lib.rr_full_route(ctypes.byref(cfg.c()), None, None, None, None, None, None) == -1
     assert rr.lib.rr_ledger_create(None, None) == -1
     assert rr.lib.rr_ledger_routes(None) is None
+
+
+def test_reserved_config_field_must_be_zero():
+    rr = _rr()
+    c = _cfg().c()
+    c.reserved = 1
+    h = ctypes.c_void_p()
+    assert rr.lib.rr_ledger_create(ctypes.byref(c), ctypes.byref(h)) == -1
+    assert not h.value
+
+
+def test_ledger_index_bytes_counts_mandatory_slots():
+    rr = _rr()
+    cfg = rr.Config(1, 1, 1024, 1024, 128, 32, 16, 16, n_sink=2, n_recent=6)
+    assert rr.index_bytes(cfg) == 1024 * (64 + 8) * 4
 
 
 def test_ledger_index_bytes_paper_figure():

@@ -274,6 +274,52 @@ def test_rollout_parity_forced_relay_path(name, kw, relay):
     assert st["compared"] >= 0.8 * st["rows"]
 
 
+# Sentinel and trigger variants (Sec. 3.1 item 3; Sec. 3.2 Eq. (8) with
+# per-row margins and the hysteresis horizon): mandatory sink and recent
+# sentinels on both relay schedules, non-causal and causal, dense and gather
+# rescoring, the wide route class, key ranges past the exact draw bitmap
+# (n_k > 4096), and the minimum reuse horizon.
+VARIANT_ROLLOUTS = [
+    ("tiny", {"n_sink": 2, "n_recent": 3, "n_layers": 5}),
+    ("tiny", {"n_sink": 1, "n_recent": 2, "causal": True, "n_layers": 5}),
+    ("drift", {"n_sink": 4, "n_recent": 4, "n_heads": 4, "n_kv_heads": 4, "n_layers": 6}),
+    ("scale", {"n_heads": 256, "n_kv_heads": 256, "n": 128, "n_sink": 2, "n_recent": 2, "n_layers": 4,
+               "anchor_every": 2}),
+    ("gqa", {"n_heads": 8, "n_kv_heads": 2, "n": 256, "n_sink": 1, "n_recent": 4, "min_reuse": 1,
+             "n_layers": 8}),
+    ("longctx", {"n_heads": 2, "n_kv_heads": 2, "n": 512, "n_sink": 2, "n_recent": 2, "n_layers": 6}),
+    ("scale", {"n": 4608, "n_heads": 1, "n_kv_heads": 1, "d": 32, "n_sink": 2, "n_recent": 3, "n_layers": 3,
+               "anchor_every": 2}),
+    ("drift", {"n_heads": 4, "n_kv_heads": 4, "n_layers": 6, "rho": 0.6, "min_reuse": 2}),
+]
+
+
+@pytest.mark.parametrize("relay", ["split", "one_pass"])
+@pytest.mark.parametrize("name,kw", VARIANT_ROLLOUTS, ids=[f"{n}-{i}" for i, (n, _) in enumerate(VARIANT_ROLLOUTS)])
+def test_rollout_parity_sentinel_variants(name, kw, relay):
+    from parity_util import rollout_compare
+    w = synth.preset(name, **kw)
+    if relay == "one_pass" and w.nk > 2048:
+        pytest.skip("the one-pass relay holds its tile's ledger bitmaps up to about 2048 key chunks")
+    note(f"variant rollout parity ({relay} relay): {name} {kw}")
+    st = rollout_compare(w, relay=relay)
+    note(f"  {st}")
+    assert st["compared"] >= 0.8 * st["rows"]
+
+
+@pytest.mark.parametrize("relay", ["split", "one_pass"])
+def test_rollout_parity_per_row_gamma(relay):
+    """Per-row guard margins gamma_i: a mix of 0, small positive, +inf and
+    -inf margins, with the reuse horizon on."""
+    from parity_util import rollout_compare
+    w = synth.preset("drift", n_heads=4, n_kv_heads=4, n_layers=6, rho=0.3, min_reuse=1, n_sink=1, n_recent=1)
+    g = np.random.default_rng(9).choice(np.array([0.0, 0.01, 0.05, math.inf, -math.inf], np.float32), size=w.rows)
+    note(f"per-row gamma rollout ({relay})")
+    st = rollout_compare(w, relay=relay, gamma_rows=g)
+    note(f"  {st}")
+    assert st["compared"] >= 0.8 * st["rows"] and st["rerouted"] > 0
+
+
 @pytest.mark.parametrize("gamma", [math.inf, -math.inf, 0.05])
 def test_forced_paths(gamma):
     """gamma = +inf refreshes every row (the relay equals full routing);
