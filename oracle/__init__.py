@@ -45,7 +45,7 @@ class _Problem(ctypes.Structure):
         ("gamma", ctypes.c_double), ("seed", ctypes.c_uint64),
         ("n_sink", ctypes.c_int32), ("n_recent", ctypes.c_int32),
         ("min_reuse", ctypes.c_int32), ("pad2_", ctypes.c_int32),
-        ("gamma_rows", ctypes.c_void_p),
+        ("gamma_rows", ctypes.c_void_p), ("k_rows", ctypes.c_void_p),
     ]
 
 
@@ -67,6 +67,7 @@ class Problem:
     n_recent: int = 0      # ... and the n_recent most recent valid chunks (Sec. 3.1, item 3)
     min_reuse: int = 0     # hysteresis: rows (re)built at layer b keep their route through b + min_reuse
     gamma_rows: object = field(default=None, compare=False)  # per-row guard margins (binary64 [rows]) or None
+    k_rows: object = field(default=None, compare=False)      # per-row route widths (int32 [rows], 1..k) or None
 
     @property
     def rows(self) -> int:
@@ -80,6 +81,10 @@ class Problem:
     def n_valid(self, i: int) -> int:
         return min(i + 1, self.n_k) if self.causal else self.n_k
 
+    def k_of(self, row: int) -> int:
+        """The route width of a row (k_i, or k)."""
+        return int(self.k_rows[row]) if self.k_rows is not None else self.k
+
     def _c(self) -> _Problem:
         g = None
         if self.gamma_rows is not None:
@@ -87,10 +92,17 @@ class Problem:
             if g.shape != (self.rows,):
                 raise ValueError("gamma_rows must have one entry per row")
             object.__setattr__(self, "_keep", g)  # (kept alive while the struct is in use)
+        kr = None
+        if self.k_rows is not None:
+            kr = np.ascontiguousarray(self.k_rows, dtype=np.int32)
+            if kr.shape != (self.rows,) or kr.min() < 1 or kr.max() > self.k:
+                raise ValueError("k_rows must hold one width in [1, k] per row")
+            object.__setattr__(self, "_keep_k", kr)
         return _Problem(self.n_heads, self.n_kv_heads, self.n_q, self.n_k, self.d, self.k,
                         self.m, self.r, int(self.causal), 0, float(self.gamma),
                         int(self.seed) & 0xFFFFFFFFFFFFFFFF, int(self.n_sink), int(self.n_recent),
-                        int(self.min_reuse), 0, None if g is None else g.ctypes.data)
+                        int(self.min_reuse), 0, None if g is None else g.ctypes.data,
+                        None if kr is None else kr.ctypes.data)
 
 
 _lib = None

@@ -59,6 +59,9 @@
  *     a row (re)built at layer b is not rerouted at layers b+1 .. b+min_reuse
  *     (0: off); the paper's optional larger margin after a refresh is left to
  *     gamma_rows, which the caller may raise for such rows;
+ *   - query-dependent budgets (Sec. 4.3-4.4): row i routes to its top k_i
+ *     chunks (k_rows[row], 1 <= k_i <= k); the near-miss set is the next m;
+ *     the route is stored in the ledger's k slots, -1 padded;
  *   - random sentinels persist until the row is next rebuilt;
  *   - score pairs: a (re)built row counts its n_i scores, a relay row counts
  *     |A| (valid candidate slots) plus n_i when it is rerouted;
@@ -87,6 +90,7 @@ typedef struct {
     int32_t min_reuse;  /* a row (re)built at layer b keeps its route at layers b+1 .. b+min_reuse */
     int32_t pad2_;
     const double *gamma_rows; /* per-row guard margins gamma_i (NULL: gamma for every row) */
+    const int32_t *k_rows;    /* per-row route widths 1 <= k_i <= k (NULL: k for every row) */
 } orc_problem;
 
 typedef struct {
@@ -184,13 +188,16 @@ static int rank_row(const orc_problem *P, const float *Q, const float *K, int h,
     return ni;
 }
 
-/* Eq. (2) with the near-miss extension of Sec. 3.1: R = the first min(k,n_i)
- * chunks in rank order, N = the next min(m, n_i - |R|); both stored sorted by
- * id and padded with -1 to widths kk and mm. */
-static void split_route(const orc_scored *work, int ni, int kk, int mm, int32_t *R, int *nR,
+/* The route width of a row: k_i when per-row budgets are given, else k. */
+static int row_k(const orc_problem *P, int64_t row) { return P->k_rows ? P->k_rows[row] : P->k; }
+
+/* Eq. (2) with the near-miss extension of Sec. 3.1: R = the first
+ * min(ki, n_i) chunks in rank order, N = the next min(m, n_i - |R|); both
+ * stored sorted by id and padded with -1 to widths kk and mm. */
+static void split_route(const orc_scored *work, int ni, int kk, int ki, int mm, int32_t *R, int *nR,
                         int32_t *N, int *nN, double *R_scores)
 {
-    int a = ni < kk ? ni : kk;
+    int a = ni < ki ? ni : ki;
     int b = (ni - a) < mm ? (ni - a) : mm;
     for (int t = 0; t < a; ++t) R[t] = work[t].id;
     qsort(R, (size_t)a, sizeof(int32_t), cmp_int);
@@ -335,7 +342,7 @@ int orc_full_route(const orc_problem *P, const float *Q, const float *K, const i
         int h = (int)(row / P->n_q), i = (int)(row % P->n_q);
         int ni = rank_row(P, Q, K, h, i, work);
         int nR;
-        split_route(work, ni, P->k, 0, routes + row * P->k, &nR, NULL, NULL,
+        split_route(work, ni, P->k, row_k(P, row), 0, routes + row * P->k, &nR, NULL, NULL,
                     route_scores ? route_scores + row * P->k : NULL);
         total += ni;
     }
@@ -356,7 +363,8 @@ int orc_route_bounds(const orc_problem *P, const float *Q, const float *K, const
         int h = (int)(row / P->n_q), i = (int)(row % P->n_q);
         int ni = rank_row(P, Q, K, h, i, work);
         const float *q = q_row(P, Q, row);
-        int ranks[4] = {P->k - 1, P->k, P->k + P->m - 1, P->k + P->m};
+        int ki = row_k(P, row);
+        int ranks[4] = {ki - 1, ki, ki + P->m - 1, ki + P->m};
         double *o = out + idx * 8;
         for (int u = 0; u < 4; ++u) {
             int rk = ranks[u];
@@ -387,7 +395,7 @@ static void rebuild_row(const orc_problem *P, int32_t layer, const float *Q, con
     int nR, nN;
     int32_t *R = routes + row * P->k;
     int32_t *C = sent + row * c;
-    split_route(work, ni, P->k, P->m, R, &nR, C, &nN, NULL);
+    split_route(work, ni, P->k, row_k(P, row), P->m, R, &nR, C, &nN, NULL);
     /* C = near-miss slots, random slots, then mandatory slots */
     memset(excl, 0, (size_t)P->n_k);
     for (int t = 0; t < nR; ++t) excl[R[t]] = 1;

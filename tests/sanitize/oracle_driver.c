@@ -15,6 +15,7 @@ typedef struct {
     uint64_t seed;
     int32_t n_sink, n_recent, min_reuse, pad2_;
     const double *gamma_rows;
+    const int32_t *k_rows;
 } orc_problem;
 
 uint64_t orc_splitmix64(uint64_t z);
@@ -46,8 +47,10 @@ static int run(int H, int Hkv, int n, int d, int k, int m, int r, int causal, in
     const int64_t rows = (int64_t)H * n;
     double *gr = malloc(sizeof(double) * (size_t)rows);
     for (int64_t t = 0; t < rows; ++t) gr[t] = (t % 3 == 0) ? INFINITY : (t % 3 == 1 ? 0.0 : 0.01);
+    int32_t *kr = malloc(sizeof(int32_t) * (size_t)rows);
+    for (int64_t t = 0; t < rows; ++t) kr[t] = 1 + (int32_t)(t % k);
     orc_problem P = {H, Hkv, n, n, d, k, m, r, causal, 0, gamma, 7, n_sink, n_recent, min_reuse, 0,
-                     per_row_gamma ? gr : NULL};
+                     per_row_gamma ? gr : NULL, per_row_gamma ? kr : NULL};
     const int c = m + r + n_sink + n_recent;
     float *Q = malloc(sizeof(float) * (size_t)(rows * d));
     float *K = malloc(sizeof(float) * (size_t)((int64_t)Hkv * n * d));
@@ -80,7 +83,7 @@ static int run(int H, int Hkv, int n, int d, int k, int m, int r, int causal, in
         P.r = r;
     }
     free(Q); free(K); free(routes); free(sent); free(build); free(age); free(mask); free(rs); free(bounds);
-    free(al); free(be); free(aa); free(ba); free(rp); free(gr);
+    free(al); free(be); free(aa); free(ba); free(rp); free(gr); free(kr);
     return bad;
 }
 
