@@ -90,6 +90,9 @@ def parse():
     ap.add_argument("--study-seeds", type=int, default=0, help="seeds of a study (0: 5 for ablation, 10 for stride)")
     ap.add_argument("--low-drift", default="0.005,0.01,0.02",
                     help="extra operating points: comma-separated rho values of the same shape ('' for none)")
+    ap.add_argument("--budgets", default="quarters",
+                    help="per-row route widths of the budgets point: 'quarters' (k/4, k/2, 3k/4, k), "
+                         "a comma list, or '' for none")
     ap.add_argument("--seeds", default="1,2", help="extra seeds for the fidelity average ('' for none)")
     ap.add_argument("--cpu-threads", type=int, default=0, help="oracle threads for cpu_baseline (0: the host's cores, at most 16)")
     return ap.parse_args()
@@ -267,6 +270,41 @@ class Schedule:
 
     def close(self):
         self.led.close()
+
+
+def operating_point(w, cfg, dev, steps):
+    """The schedule and its full-routing baseline on another operating point of
+    the workload (a drift level, per-row widths): median relay-layer rate,
+    schedule and baseline rates, fidelity and per-kernel durations."""
+    import torch
+    from paper_2609_07306_amd import routerelay as rr
+    rows, L = cfg.rows, w.n_layers
+    relay_l = [l for l in range(L) if not w.is_anchor(l)]
+    q, k_, _ = upload(w, dev)
+    S = Schedule(w, cfg, q, k_, dev)
+    S.relay_step()
+    S.full_step()
+    ms_l, _ = S.timed(S.relay_step, steps)
+    ms_f, _ = S.timed(S.full_step, steps)
+    lay = S.layer_times(steps)
+    rr.profile_start()
+    S.relay_step()
+    pr = rr.profile_stop()
+    fl = S.fidelity(run_full=True)
+    rel = lay[:, relay_l].ravel()
+    S.close()
+    del q, k_, S
+    torch.cuda.empty_cache()
+    return {
+        "rerouted_frac_relay_layers": round(fl["rerouted_frac_relay_layers"], 4),
+        "recall": round(fl["recall"], 6),
+        "score_pair_frac": round(fl["score_pair_frac"], 4),
+        "relay_layer_rows_per_s": round(rows / (1e-3 * pct(rel, 50)), 1),
+        "full_route_rows_per_s": round(rows * L / (ms_f * 1e-3), 1),
+        "relay_vs_full_layer": round((ms_f / L) / pct(rel, 50), 3),
+        "schedule_rows_per_s": round(rows * L / (ms_l * 1e-3), 1),
+        "kernel_us": {kk: round(1e3 * t / n, 2) for kk, (t, n) in pr.items() if n},
+    }
 
 
 def measured_peaks(dev):
@@ -625,41 +663,25 @@ def main():
                                  "per_seed": {str(s_): {kk: round(per_seed[s_][kk], 6) for kk in keys} for s_ in sorted(per_seed)}}
 
     # ---- low-drift operating points of the same shape (the method's regime)
+    steps_op = max(3, min(args.steps, 5))
     pts = [float(x) for x in args.low_drift.split(",") if x.strip()]
     if pts and args.rho is None:
         low = []
         for rho in pts:
             wl = w.with_(rho=rho)
             print(f"[bench] low-drift point rho={rho}", file=sys.stderr, flush=True)
-            q, k_, _ = upload(wl, dev)
             cl = dataclasses.replace(rr.Config.of(wl), relay=args.relay)
-            Sl = Schedule(wl, cl, q, k_, dev)
-            Sl.relay_step()
-            Sl.full_step()
-            steps_l = max(3, min(args.steps, 5))
-            ms_l, _ = Sl.timed(Sl.relay_step, steps_l)
-            ms_f, _ = Sl.timed(Sl.full_step, steps_l)
-            lay_l = Sl.layer_times(steps_l)
-            rr.profile_start()
-            Sl.relay_step()
-            pr = rr.profile_stop()
-            fl = Sl.fidelity(run_full=True)
-            rel = lay_l[:, relay_l].ravel()
-            low.append({
-                "rho": rho,
-                "rerouted_frac_relay_layers": round(fl["rerouted_frac_relay_layers"], 4),
-                "recall": round(fl["recall"], 6),
-                "score_pair_frac": round(fl["score_pair_frac"], 4),
-                "relay_layer_rows_per_s": round(rows / (1e-3 * pct(rel, 50)), 1),
-                "full_route_rows_per_s": round(rows * L / (ms_f * 1e-3), 1),
-                "relay_vs_full_layer": round((ms_f / L) / pct(rel, 50), 3),
-                "schedule_rows_per_s": round(rows * L / (ms_l * 1e-3), 1),
-                "kernel_us": {k_: round(1e3 * t / n, 2) for k_, (t, n) in pr.items() if n},
-            })
-            Sl.close()
-            del q, k_
-            torch.cuda.empty_cache()
+            low.append({"rho": rho, **operating_point(wl, cl, dev, steps_op)})
         out["low_drift"] = low
+
+    # ---- query-dependent route budgets: per-row widths, one launch for all
+    if args.budgets:
+        widths = None if args.budgets == "quarters" else [int(x) for x in args.budgets.split(",")]
+        kr = synth.route_budgets(w, widths)
+        print(f"[bench] route budgets {sorted(set(kr.tolist()))}", file=sys.stderr, flush=True)
+        cb = dataclasses.replace(cfg, k_rows=torch.from_numpy(kr).to(dev))
+        out["budgets"] = {"widths": sorted(set(kr.tolist())), "mean_width": round(float(kr.mean()), 3),
+                          **operating_point(w, cb, dev, steps_op)}
 
     # ---- measured peaks beside the nominal ones
     mp = measured_peaks(dev)

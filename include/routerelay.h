@@ -109,6 +109,14 @@ typedef struct {
      * layers, e.g. to raise the margin of recently refreshed rows); NULL: the
      * scalar gamma for every row.  Values must not be NaN. */
     const float *gamma_rows;
+    /* Query-dependent route budgets (Sec. 4.3): a device array of H_q*n_q
+     * int32 route widths k_i, read by every routing call (full, anchor,
+     * relay).  Row i routes to its k_i best chunks, in its first k_i route
+     * slots (the other k - k_i are -1), and its near-miss sentinels are the m
+     * chunks ranked after them.  Rows of every width share the launches (one
+     * bucket).  Values outside [1, k] are clamped to it.  NULL: k for every
+     * row. */
+    const int32_t *k_rows;
 } rr_config;
 
 typedef struct rr_ledger rr_ledger;

@@ -352,7 +352,8 @@ int orc_full_route(const orc_problem *P, const float *Q, const float *K, const i
 }
 
 /* Boundary scores used to classify near-ties: for each row the scores at
- * rank k, k+1, k+m and k+m+1 (1-based; NaN where the rank does not exist),
+ * rank k_i, k_i+1, k_i+m and k_i+m+1 (1-based, k_i the row's route width;
+ * NaN where the rank does not exist),
  * followed by sum_t |q_t k_t| of the same four chunks.  out is [rows, 8]. */
 int orc_route_bounds(const orc_problem *P, const float *Q, const float *K, const int64_t *rows,
                      int64_t n_rows, double *out)

@@ -288,6 +288,7 @@ rr::RouteArgs route_args(const rr_config &c, const void *Q, const void *K)
     a.n_recent = c.n_recent;
     a.min_reuse = c.min_reuse;
     a.gamma_rows = c.gamma_rows;
+    a.k_rows = c.k_rows;
     a.causal = c.causal;
     a.tile_rows = rr::route_tile_rows(c.k + c.m, c.n_heads, c.n_q);
     a.tiles_per_head = (c.n_q + a.tile_rows - 1) / a.tile_rows;

@@ -30,6 +30,7 @@ struct RouteArgs {
     int32_t n_sink, n_recent;  // mandatory sentinels (sentinel slots: m near-miss, r random, n_sink + n_recent mandatory)
     int32_t min_reuse;         // relay: minimum reuse horizon in layers (0: none)
     const float *gamma_rows;   // relay: per-row guard margins, or null (gamma for every row)
+    const int32_t *k_rows;     // per-row route widths in [1, k] (clamped), or null (k for every row)
     int32_t causal;
     int32_t layer;
     int32_t mode;

@@ -42,7 +42,7 @@ class _Config(ctypes.Structure):
         ("r", ctypes.c_int32), ("dtype", ctypes.c_int32), ("causal", ctypes.c_int32),
         ("gamma", ctypes.c_float), ("options", ctypes.c_uint32), ("seed", ctypes.c_uint64),
         ("n_sink", ctypes.c_int32), ("n_recent", ctypes.c_int32), ("min_reuse", ctypes.c_int32),
-        ("reserved", ctypes.c_int32), ("gamma_rows", ctypes.c_void_p),
+        ("reserved", ctypes.c_int32), ("gamma_rows", ctypes.c_void_p), ("k_rows", ctypes.c_void_p),
     ]
 
 
@@ -108,6 +108,7 @@ class Config:
     n_recent: int = 0    # ... and recent chunks
     min_reuse: int = 0   # minimum reuse horizon (layers)
     gamma_rows: object = None  # per-row guard margins: float32 device tensor [rows], or None
+    k_rows: object = None      # per-row route widths in [1, k]: int32 device tensor [rows], or None
 
     @property
     def rows(self) -> int:
@@ -124,11 +125,17 @@ class Config:
             if t.dtype != torch.float32 or tuple(t.shape) != (self.rows,):
                 raise ValueError("gamma_rows must be a float32 tensor with one entry per row")
             g = _ptr(t)
+        kr = None
+        if self.k_rows is not None:
+            t = self.k_rows
+            if t.dtype != torch.int32 or tuple(t.shape) != (self.rows,):
+                raise ValueError("k_rows must be an int32 tensor with one entry per row")
+            kr = _ptr(t)
         return _Config(self.n_heads, self.n_kv_heads, self.n_q, self.n_k, self.d, self.k, self.m,
                        self.r, RR_BF16 if self.dtype == "bf16" else RR_F32, int(self.causal),
                        float(self.gamma), _RELAY_OPTIONS[self.relay],
                        int(self.seed) & 0xFFFFFFFFFFFFFFFF, int(self.n_sink), int(self.n_recent),
-                       int(self.min_reuse), 0, g)
+                       int(self.min_reuse), 0, g, kr)
 
     @staticmethod
     def of(w) -> "Config":

@@ -21,6 +21,10 @@ with PCG64):
 8. near-tie workloads, at every layer after the drift step:
    ``K[dup] = K[src] + 1e-3 eta`` with ``eta ~ N(0, I_d)``.
 
+Query-dependent route budgets (``route_budgets``) come from a stream of their
+own, ``default_rng([seed, 7])``: each row draws one of a few widths (buckets)
+uniformly.
+
 bf16 workloads round the binary32 draw to bf16 with round-to-nearest-even; the
 GPU reads those bits and the oracle reads the same values widened exactly to
 binary32.
@@ -101,6 +105,19 @@ def preset(name: str, **kw) -> Workload:
     else:
         raise KeyError(name)
     return w.with_(**kw) if kw else w
+
+
+def route_budgets(w: Workload, widths=None) -> np.ndarray:
+    """Per-row route widths k_i (int32 [rows], head-major like the rows): one
+    of ``widths`` per row, uniformly; by default the four buckets k/4, k/2,
+    3k/4 and k (at least 1)."""
+    if widths is None:
+        widths = sorted({max(1, (w.k * q) // 4) for q in (1, 2, 3, 4)})
+    widths = np.asarray(widths, dtype=np.int32)
+    if widths.min() < 1 or widths.max() > w.k:
+        raise ValueError("route widths must lie in [1, k]")
+    rng = np.random.default_rng([w.seed, 7])
+    return widths[rng.integers(0, len(widths), size=w.rows)].astype(np.int32)
 
 
 def bf16_round(x: np.ndarray) -> np.ndarray:

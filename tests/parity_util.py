@@ -102,10 +102,11 @@ def n_valid_rows(p):
     return np.minimum(i + 1, p.n_k) if p.causal else np.full(p.rows, p.n_k)
 
 
-def rollout_compare(w, gamma=None, check_scores=True, relay="auto", gamma_rows=None):
+def rollout_compare(w, gamma=None, check_scores=True, relay="auto", gamma_rows=None, k_rows=None):
     """Runs the workload's anchor/relay schedule on the GPU and on the oracle
     (relay: the relay schedule, "auto", "one_pass" or "split"; gamma_rows:
-    per-row guard margins, binary32 values, or None).
+    per-row guard margins, binary32 values, or None; k_rows: per-row route
+    widths in [1, k], or None).
 
     Returns a dict of statistics; raises AssertionError on any mismatch of a
     trusted row."""
@@ -117,6 +118,10 @@ def rollout_compare(w, gamma=None, check_scores=True, relay="auto", gamma_rows=N
         g32 = np.ascontiguousarray(gamma_rows, dtype=np.float32)
         p = dataclasses.replace(p, gamma_rows=g32.astype(np.float64))
         cfg = dataclasses.replace(cfg, gamma_rows=torch.from_numpy(g32).to(torch.device("cuda", torch.cuda.current_device())))
+    if k_rows is not None:
+        k32 = np.ascontiguousarray(k_rows, dtype=np.int32)
+        p = dataclasses.replace(p, k_rows=k32)
+        cfg = dataclasses.replace(cfg, k_rows=torch.from_numpy(k32).to(torch.device("cuda", torch.cuda.current_device())))
     L = rr.Ledger(cfg)
     ref = oracle.new_ledger(p)
     trusted = np.zeros(p.rows, dtype=bool)

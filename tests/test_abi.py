@@ -39,10 +39,10 @@ def test_library_exports_every_declared_symbol():
 
 def test_config_struct_layout():
     rr = _rr()
-    assert ctypes.sizeof(rr._Config) == 80
+    assert ctypes.sizeof(rr._Config) == 88
     assert rr._Config.seed.offset == 48 and rr._Config.gamma.offset == 40
     assert rr._Config.n_sink.offset == 56 and rr._Config.reserved.offset == 68
-    assert rr._Config.gamma_rows.offset == 72
+    assert rr._Config.gamma_rows.offset == 72 and rr._Config.k_rows.offset == 80
 
 
 def test_status_strings():
