@@ -242,7 +242,10 @@ typedef enum {
     RR_KERNEL_REROUTE = 2,  /* GEMM + TopK + ledger build, compacted rows */
     RR_KERNEL_RESCORE = 3,  /* rescoring (dense tiles or gather), trigger, compaction counts, ages */
     RR_KERNEL_RELAY = 4,    /* one-pass relay: rescoring + trigger + GEMM + TopK + ledger build of the flagged rows */
-    RR_KERNEL_KINDS = 5
+    RR_KERNEL_POOL = 5,     /* chunk pooling */
+    RR_KERNEL_EXPAND = 6,   /* token expansion */
+    RR_KERNEL_ATTENTION = 7, /* sparse attention over routed chunks */
+    RR_KERNEL_KINDS = 8
 } rr_kernel_kind;
 
 rr_status rr_profile_start(void);
@@ -272,6 +275,60 @@ const char *rr_status_string(rr_status status);
 
 /* Message of the calling thread's most recent failure ("" if none). */
 const char *rr_last_error(void);
+
+/* ------------------------------------------------------------------------
+ * The steps either side of route maintenance.  Chunks are consecutive runs of
+ * `chunk` tokens, the last one possibly shorter: n_chunks =
+ * ceil(n_tokens / chunk), chunk j holds tokens j*chunk .. min((j+1)*chunk,
+ * n_tokens) - 1.  All pointers are device memory; every call enqueues on the
+ * given HIP stream (NULL: the default stream) and returns.
+ * ---------------------------------------------------------------------- */
+
+/* Chunk representations (Sec. 2.1: the router forms one representation per
+ * chunk of tokens; here the mean of the chunk's token vectors).  X is
+ * [n_heads, n_tokens, d] of dtype (rr_dtype), Xc receives [n_heads, n_chunks,
+ * d] of the same dtype: each chunk's mean, summed in binary32 and rounded to
+ * nearest even for bf16.  d a multiple of 8, at most 1024; chunk >= 1.
+ * Returns RR_ERR_INVALID for bad sizes or NULL pointers. */
+rr_status rr_pool_chunks(const void *X, int32_t n_heads, int32_t n_tokens, int32_t d, int32_t chunk,
+                         int32_t dtype, void *Xc, void *hip_stream);
+
+/* Token expansion (Sec. 2.1: selected chunks are expanded into token
+ * indices).  routes is [rows, k] chunk ids (a ledger's or rr_full_route's
+ * layout), tokens receives [rows, k*chunk] int32: route slot s fills columns
+ * s*chunk .. s*chunk + chunk - 1 with its chunk's token ids ascending, -1
+ * past the sequence's last token and for an empty (-1) or out-of-range slot.
+ * Returns RR_ERR_INVALID for bad sizes or NULL pointers. */
+rr_status rr_expand_tokens(const int32_t *routes, int64_t rows, int32_t k, int32_t chunk, int32_t n_tokens,
+                           int32_t *tokens, void *hip_stream);
+
+/* Sparse attention over routed chunks (Sec. 2.2 Eq. (3)): every query token t
+ * of chunk i of head h attends, with one softmax scaled by `scale`, to the
+ * tokens of the chunks in row h*n_chunks + i of routes; when causal, keys
+ * after t are excluded (and routed chunks after i contribute nothing).  Slots
+ * holding -1 or an id outside [0, n_chunks) are skipped; a query with no
+ * admissible key gets a zero output.  Query head h reads key / value head
+ * h / (n_heads / n_kv_heads).  Layouts: Q and O [n_heads, n_tokens, d], K and
+ * V [n_kv_heads, n_tokens, d], bf16, row-major; routes [n_heads*n_chunks, k]
+ * int32.  Scores and sums in binary32, the softmax weights rounded to bf16
+ * for the value product, O rounded to nearest even.  Supported: bf16 with
+ * d = 64 or 128, 1 <= k <= 256.  Returns RR_ERR_INVALID for bad sizes or NULL
+ * pointers, RR_ERR_UNSUPPORTED for other dtypes or d. */
+typedef struct {
+    int32_t n_heads;
+    int32_t n_kv_heads;
+    int32_t n_tokens;
+    int32_t d;
+    int32_t chunk;      /* tokens per chunk */
+    int32_t k;          /* route slots per row */
+    int32_t causal;     /* 1: key token u is visible to query token t iff u <= t */
+    int32_t dtype;      /* rr_dtype of Q, K, V and O (RR_BF16) */
+    float scale;        /* softmax scale; 0: 1/sqrt(d) */
+    int32_t reserved;   /* must be 0 */
+} rr_attn_config;
+
+rr_status rr_sparse_attention(const rr_attn_config *cfg, const void *Q, const void *K, const void *V,
+                              const int32_t *routes, void *O, void *hip_stream);
 
 #ifdef __cplusplus
 }

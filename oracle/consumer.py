@@ -72,12 +72,13 @@ def sparse_attention(Q, K, V, routes, chunk, causal, scale=None, rows=None):
     nc = n_chunks(n, chunk)
     if scale is None:
         scale = 1.0 / math.sqrt(d)
-    tok = expand_tokens(np.asarray(routes, np.int32), chunk, n)
+    routes = np.asarray(routes)
 
     def one(h, t):
         i = t // chunk
-        u = tok[h * nc + i]
-        u = u[u >= 0]
+        # the tokens of the row's admissible route slots, slot by slot
+        parts = [np.arange(j * chunk, min((j + 1) * chunk, n)) for j in routes[h * nc + i].tolist() if 0 <= j < nc]
+        u = np.concatenate(parts) if parts else np.zeros(0, np.int64)
         if causal:
             u = u[u <= t]
         if len(u) == 0:

@@ -17,7 +17,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "librouterelay.so")
-SOURCES = ["rr_api.hip", "rr_route.hip", "rr_rescore.hip", "rr_rescore_dense.hip"] + [
+SOURCES = ["rr_api.hip", "rr_route.hip", "rr_rescore.hip", "rr_rescore_dense.hip", "rr_consumer.hip"] + [
     f"rr_route_{t}_{m}.hip" for t in ("f32", "bf16") for m in ("full", "anchor", "reroute", "relay")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -835,3 +835,71 @@ rr_status rr_set_sweep_cap(int32_t cap)
 }
 
 }  // extern "C"
+
+// ------------------------------------------------- either side of the path
+
+rr_status rr_pool_chunks(const void *X, int32_t n_heads, int32_t n_tokens, int32_t d, int32_t chunk,
+                         int32_t dtype, void *Xc, void *hip_stream)
+{
+    if (!X || !Xc) return fail(RR_ERR_INVALID, "X and Xc must be device pointers");
+    if (n_heads < 1 || n_tokens < 1 || chunk < 1) return fail(RR_ERR_INVALID, "n_heads, n_tokens and chunk must be >= 1");
+    if (d < 8 || d > 1024 || d % 8 != 0) return fail(RR_ERR_INVALID, "d must be a multiple of 8 in [8, 1024]");
+    if (dtype != RR_F32 && dtype != RR_BF16) return fail(RR_ERR_INVALID, "unknown dtype");
+    hipStream_t stream = reinterpret_cast<hipStream_t>(hip_stream);
+    hipError_t e = timed(RR_KERNEL_POOL, stream,
+                         [&] { return rr::launch_pool(X, n_heads, n_tokens, d, chunk, dtype, Xc, stream); });
+    return e == hipSuccess ? RR_OK : hip_fail(e, "pooling launch");
+}
+
+rr_status rr_expand_tokens(const int32_t *routes, int64_t rows, int32_t k, int32_t chunk, int32_t n_tokens,
+                           int32_t *tokens, void *hip_stream)
+{
+    if (!routes || !tokens) return fail(RR_ERR_INVALID, "routes and tokens must be device pointers");
+    if (rows < 1 || k < 1 || chunk < 1 || n_tokens < 1)
+        return fail(RR_ERR_INVALID, "rows, k, chunk and n_tokens must be >= 1");
+    if ((int64_t)k * chunk > INT32_MAX) return fail(RR_ERR_INVALID, "k * chunk beyond int32");
+    hipStream_t stream = reinterpret_cast<hipStream_t>(hip_stream);
+    hipError_t e = timed(RR_KERNEL_EXPAND, stream,
+                         [&] { return rr::launch_expand(routes, rows, k, chunk, n_tokens, tokens, stream); });
+    return e == hipSuccess ? RR_OK : hip_fail(e, "expansion launch");
+}
+
+rr_status rr_sparse_attention(const rr_attn_config *cfg, const void *Q, const void *K, const void *V,
+                              const int32_t *routes, void *O, void *hip_stream)
+{
+    if (!cfg) return fail(RR_ERR_INVALID, "config is NULL");
+    const rr_attn_config &c = *cfg;
+    if (!Q || !K || !V || !routes || !O) return fail(RR_ERR_INVALID, "Q, K, V, routes and O must be device pointers");
+    if (c.n_heads < 1 || c.n_kv_heads < 1 || c.n_heads % c.n_kv_heads != 0)
+        return fail(RR_ERR_INVALID, "n_heads must be a positive multiple of n_kv_heads");
+    if (c.n_tokens < 1 || c.chunk < 1) return fail(RR_ERR_INVALID, "n_tokens and chunk must be >= 1");
+    if (c.k < 1 || c.k > rr::kMaxAttnSlots) return fail(RR_ERR_INVALID, "k must lie in [1, 256]");
+    if (c.causal != 0 && c.causal != 1) return fail(RR_ERR_INVALID, "causal must be 0 or 1");
+    if (c.reserved != 0) return fail(RR_ERR_INVALID, "rr_attn_config.reserved must be 0");
+    if (!(c.scale >= 0.f) || std::isinf(c.scale)) return fail(RR_ERR_INVALID, "scale must be finite and >= 0");
+    if (c.dtype != RR_F32 && c.dtype != RR_BF16) return fail(RR_ERR_INVALID, "unknown dtype");
+    if (!rr::attention_supported(c.dtype, c.d))
+        return fail(RR_ERR_UNSUPPORTED, "sparse attention supports bf16 with d = 64 or 128");
+    rr::AttnArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.Q = Q;
+    a.K = K;
+    a.V = V;
+    a.O = O;
+    a.routes = routes;
+    a.n_heads = c.n_heads;
+    a.n_kv_heads = c.n_kv_heads;
+    a.n_tokens = c.n_tokens;
+    a.d = c.d;
+    a.chunk = c.chunk;
+    a.k = c.k;
+    a.causal = c.causal;
+    a.n_chunks = (int32_t)(((int64_t)c.n_tokens + c.chunk - 1) / c.chunk);
+    a.tiles_per_chunk = rr::attention_tiles_per_chunk(c.chunk < c.n_tokens ? c.chunk : c.n_tokens);
+    a.scale = c.scale > 0.f ? c.scale : 1.f / std::sqrt((float)c.d);
+    if ((int64_t)c.n_heads * a.n_chunks * a.tiles_per_chunk > INT32_MAX)
+        return fail(RR_ERR_INVALID, "too many query tiles");
+    hipStream_t stream = reinterpret_cast<hipStream_t>(hip_stream);
+    hipError_t e = timed(RR_KERNEL_ATTENTION, stream, [&] { return rr::launch_attention(a, stream); });
+    return e == hipSuccess ? RR_OK : hip_fail(e, "attention launch");
+}

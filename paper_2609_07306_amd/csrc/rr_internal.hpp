@@ -91,6 +91,26 @@ inline hipError_t raise_lds_limit(const void *fn, size_t lds, LdsLimit &seen)
 }
 
 
+// Sparse attention over routed chunks (rr_consumer.hip).
+constexpr int kMaxAttnSlots = 256;  // route slots per row
+
+struct AttnArgs {
+    const void *Q, *K, *V;  // bf16 [H, n_tokens, d], [H_kv, n_tokens, d] x2
+    void *O;                // bf16 [H, n_tokens, d]
+    const int32_t *routes;  // [H * n_chunks, k]
+    int32_t n_heads, n_kv_heads, n_tokens, d, chunk, k, causal;
+    int32_t n_chunks, tiles_per_chunk;
+    float scale;
+};
+
+bool attention_supported(int dtype, int d);
+int attention_tiles_per_chunk(int chunk);
+hipError_t launch_attention(const AttnArgs &a, hipStream_t stream);
+hipError_t launch_pool(const void *X, int n_heads, int n_tok, int d, int chunk, int dtype, void *out,
+                       hipStream_t stream);
+hipError_t launch_expand(const int32_t *routes, int64_t rows, int k, int chunk, int n_tok, int32_t *tokens,
+                         hipStream_t stream);
+
 // Supported (dtype, d) combinations; dtype 0 = binary32, 1 = bf16.
 bool route_supported(int dtype, int d, int T);
 int route_tile_rows(int T, int n_heads, int n_q);  // query rows per route tile for T = k + m

@@ -25,8 +25,9 @@ EXPORTED = (
     "rr_ledger_routes", "rr_ledger_export", "rr_ledger_import", "rr_ledger_relay_stats",
     "rr_ledger_index_bytes", "rr_status_string", "rr_last_error", "rr_profile_start",
     "rr_profile_stop", "rr_unconverged_rows", "rr_set_sweep_cap", "rr_relay_layer_static",
+    "rr_pool_chunks", "rr_expand_tokens", "rr_sparse_attention",
 )
-KERNEL_KINDS = ("full", "anchor", "reroute", "rescore", "relay")
+KERNEL_KINDS = ("full", "anchor", "reroute", "rescore", "relay", "pool", "expand", "attention")
 
 
 class RRError(RuntimeError):
@@ -43,6 +44,14 @@ class _Config(ctypes.Structure):
         ("gamma", ctypes.c_float), ("options", ctypes.c_uint32), ("seed", ctypes.c_uint64),
         ("n_sink", ctypes.c_int32), ("n_recent", ctypes.c_int32), ("min_reuse", ctypes.c_int32),
         ("reserved", ctypes.c_int32), ("gamma_rows", ctypes.c_void_p), ("k_rows", ctypes.c_void_p),
+    ]
+
+
+class _AttnConfig(ctypes.Structure):
+    _fields_ = [
+        ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("n_tokens", ctypes.c_int32),
+        ("d", ctypes.c_int32), ("chunk", ctypes.c_int32), ("k", ctypes.c_int32), ("causal", ctypes.c_int32),
+        ("dtype", ctypes.c_int32), ("scale", ctypes.c_float), ("reserved", ctypes.c_int32),
     ]
 
 
@@ -69,6 +78,9 @@ def _load():
         "rr_unconverged_rows": (ctypes.c_int, [ctypes.POINTER(ctypes.c_uint64)]),
         "rr_set_sweep_cap": (ctypes.c_int, [i32]),
         "rr_relay_layer_static": (ctypes.c_int, [cfgp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+        "rr_pool_chunks": (ctypes.c_int, [vp, i32, i32, i32, i32, i32, vp, vp]),
+        "rr_expand_tokens": (ctypes.c_int, [vp, ctypes.c_int64, i32, i32, i32, vp, vp]),
+        "rr_sparse_attention": (ctypes.c_int, [ctypes.POINTER(_AttnConfig), vp, vp, vp, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -313,3 +325,58 @@ def to_device(x_dev, dtype: str, device="cuda"):
     else:
         t = torch.from_numpy(np.ascontiguousarray(x_dev, dtype=np.float32))
     return t.to(device)
+
+
+# ------------------------------------------------- either side of the path
+
+def n_chunks(n_tokens: int, chunk: int) -> int:
+    return -(-n_tokens // chunk)
+
+
+def pool_chunks(X, chunk: int, out=None, stream=None):
+    """rr_pool_chunks: X [H, n_tokens, d] (float32 or bfloat16 device tensor)
+    -> [H, n_chunks, d] chunk means of the same dtype."""
+    if X.dim() != 3 or X.dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError("X must be a [H, n_tokens, d] float32 or bfloat16 tensor")
+    H, n, d = X.shape
+    shape = (H, n_chunks(n, chunk), d)
+    if out is None:
+        out = torch.empty(shape, dtype=X.dtype, device=X.device)
+    dt = RR_BF16 if X.dtype == torch.bfloat16 else RR_F32
+    _check(lib.rr_pool_chunks(_ptr(X), H, n, d, chunk, dt, _out(out, shape, X.dtype), _stream(stream)))
+    return out
+
+
+def expand_tokens(routes, chunk: int, n_tokens: int, out=None, stream=None):
+    """rr_expand_tokens: routes [rows, k] int32 -> token ids [rows, k*chunk]."""
+    if routes.dim() != 2 or routes.dtype != torch.int32:
+        raise TypeError("routes must be a [rows, k] int32 tensor")
+    rows, k = routes.shape
+    shape = (rows, k * chunk)
+    if out is None:
+        out = torch.empty(shape, dtype=torch.int32, device=routes.device)
+    _check(lib.rr_expand_tokens(_ptr(routes), rows, k, chunk, n_tokens, _out(out, shape, torch.int32),
+                                _stream(stream)))
+    return out
+
+
+def sparse_attention(Q, K, V, routes, chunk: int, causal: bool, scale: float = 0.0, out=None, stream=None):
+    """rr_sparse_attention: Q [H, n, d], K and V [H_kv, n, d] bfloat16,
+    routes [H * n_chunks, k] int32 -> O [H, n, d] bfloat16."""
+    for t in (Q, K, V):
+        if t.dim() != 3 or t.dtype != torch.bfloat16:
+            raise TypeError("Q, K and V must be 3-d bfloat16 tensors")
+    H, n, d = Q.shape
+    Hkv = K.shape[0]
+    if tuple(K.shape) != (Hkv, n, d) or tuple(V.shape) != (Hkv, n, d):
+        raise ValueError("K and V must be [H_kv, n_tokens, d]")
+    nc = n_chunks(n, chunk)
+    if routes.dim() != 2 or routes.dtype != torch.int32 or routes.shape[0] != H * nc:
+        raise ValueError("routes must be [H * n_chunks, k] int32")
+    if out is None:
+        out = torch.empty_like(Q)
+    cfg = _AttnConfig(H, Hkv, n, d, chunk, routes.shape[1], int(causal), RR_BF16, float(scale), 0)
+    _check(lib.rr_sparse_attention(ctypes.byref(cfg), _ptr(Q), _ptr(K), _ptr(V), _ptr(routes),
+                                   _out(out, (H, n, d), torch.bfloat16), _stream(stream)))
+    return out
+
