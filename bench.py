@@ -81,7 +81,7 @@ def parse():
     ap.add_argument("--no-full", action="store_true", help="skip the full-routing baseline")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a device-to-device copy of MIB MiB (calibrates the HBM byte counters)")
-    ap.add_argument("--counter-pass", default="", choices=("", "full", "anchor", "relay"),
+    ap.add_argument("--counter-pass", default="", choices=("", "full", "anchor", "relay", "attention"),
                     help="only launch this call 5 times on the workload's first layers (a program for "
                          "rocprofv3 counter passes) and exit")
     ap.add_argument("--study", default="", choices=("", "ablation", "stride"),
@@ -93,6 +93,10 @@ def parse():
     ap.add_argument("--budgets", default="quarters",
                     help="per-row route widths of the budgets point: 'quarters' (k/4, k/2, 3k/4, k), "
                          "a comma list, or '' for none")
+    ap.add_argument("--prefill-layers", type=int, default=8,
+                    help="layers of the prefill point (pooling + routing + sparse attention on the causal GQA "
+                         "prefill shape); 0 for none")
+    ap.add_argument("--prefill-only", action="store_true", help="run only the prefill point and print it")
     ap.add_argument("--seeds", default="1,2", help="extra seeds for the fidelity average ('' for none)")
     ap.add_argument("--cpu-threads", type=int, default=0, help="oracle threads for cpu_baseline (0: the host's cores, at most 16)")
     return ap.parse_args()
@@ -418,6 +422,136 @@ def run_policy(w, dev, policy="relay", stride=4):
     return {"recall": hit / tot, "rerouted": rer / (rows * L), "score_pairs": sp / fp}
 
 
+def prefill(dev, n_layers, steps=2):
+    """The route-maintenance path inside a prefill: per layer, pooling of the
+    query and key tokens into chunk representations, routing (RouteRelay's
+    anchor / relay schedule, or full routing), and sparse attention over the
+    routed chunks' tokens.  Shape: the causal GQA prefill (131072 tokens in
+    256-token chunks, 32 query heads on 8 key heads, d = 128, bf16, top-32
+    with 16 near-miss and 16 random sentinels), anchor at layer 0.
+
+    Tokens: the chunk representations of the gqa workload (its drift across
+    layers) repeated over each chunk's 256 tokens plus N(0, 0.25/d) token
+    noise, values N(0, 1/d); generated on the device per layer, outside the
+    timed events.  Returns per-layer durations (HIP events around the library
+    calls on the stream), the attention kernel's MFMA rate, and the layer
+    time with RouteRelay against full routing."""
+    import numpy as np
+    import torch
+    from paper_2609_07306_amd import routerelay as rr
+    from paper_2609_07306_amd import synth
+    w = synth.preset("gqa", n_layers=n_layers, anchor_every=0)
+    chunk, d, H, Hkv, nc = 256, w.d, w.n_heads, w.n_kv_heads, w.n
+    n = nc * chunk
+    cfg = rr.Config.of(w)
+    lay = synth.layers(w)
+
+    def tokens(layer):
+        g = torch.Generator(device=dev).manual_seed(1000 + layer)
+        Qc = rr.to_device(lay[layer][2], "bf16", dev).float()
+        Kc = rr.to_device(lay[layer][3], "bf16", dev).float()
+        sig = 0.5 / d ** 0.5
+        Q = (Qc.repeat_interleave(chunk, 1) + sig * torch.randn((H, n, d), generator=g, device=dev)).to(torch.bfloat16)
+        K = (Kc.repeat_interleave(chunk, 1) + sig * torch.randn((Hkv, n, d), generator=g, device=dev)).to(torch.bfloat16)
+        V = (torch.randn((Hkv, n, d), generator=g, device=dev) / d ** 0.5).to(torch.bfloat16)
+        return Q, K, V
+
+    def run(policy):
+        led = rr.Ledger(cfg)
+        routes = torch.empty((H * nc, w.k), dtype=torch.int32, device=dev)
+        O = torch.empty((H, n, d), dtype=torch.bfloat16, device=dev)
+        per = np.zeros((steps, n_layers, 3))
+        pairs_attn = np.zeros(n_layers)
+        rer = np.zeros(n_layers)
+        mask = torch.zeros(H * nc, dtype=torch.uint8, device=dev)
+        for st in range(steps):
+            for l in range(n_layers):
+                Q, K, V = tokens(l)
+                torch.cuda.synchronize()
+                ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+                ev[0].record()
+                Qc, Kc = rr.pool_chunks(Q, chunk), rr.pool_chunks(K, chunk)
+                ev[1].record()
+                if policy == "full":
+                    rr.full_route(cfg, Qc, Kc, routes)
+                elif l == 0:
+                    led.anchor(l, Qc, Kc, routes=routes)
+                else:
+                    led.relay(l, Qc, Kc, routes=routes, mask=mask)
+                ev[2].record()
+                rr.sparse_attention(Q, K, V, routes, chunk, True, out=O)
+                ev[3].record()
+                torch.cuda.synchronize()
+                per[st, l] = [ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2]), ev[2].elapsed_time(ev[3])]
+                if st == 0:
+                    # admitted (query, key) pairs: a routed chunk j < i gives chunk^2,
+                    # the diagonal chunk chunk*(chunk+1)/2
+                    i = torch.arange(nc, device=dev).repeat(H).unsqueeze(1)
+                    ok = routes >= 0
+                    full = (ok & (routes < i)).sum().item()
+                    diag = (ok & (routes == i)).sum().item()
+                    pairs_attn[l] = full * chunk * chunk + diag * chunk * (chunk + 1) / 2
+                    rer[l] = H * nc if (policy == "full" or l == 0) else int(mask.sum().item())
+                del Q, K, V
+        led.close()
+        return per.mean(0), pairs_attn, rer
+
+    print("[bench] prefill point: RouteRelay schedule", file=sys.stderr, flush=True)
+    relay_t, pairs, rer = run("relay")
+    print("[bench] prefill point: full routing", file=sys.stderr, flush=True)
+    full_t, _, _ = run("full")
+    attn_us = 1e3 * relay_t[:, 2]
+    attn_tflops = 4.0 * d * pairs / (attn_us * 1e-6) / 1e12
+    pool_bytes = (H + Hkv) * n * d * 2 + (H + Hkv) * nc * d * 2
+    relay_layers = list(range(1, n_layers))
+    lt_relay = relay_t.sum(1)
+    lt_full = full_t.sum(1)
+    return {
+        "shape": f"causal GQA prefill: {n} tokens in {chunk}-token chunks ({nc} chunks), {H} query heads on "
+                 f"{Hkv} key heads, d={d}, bf16, k={w.k}, m={w.m}, r={w.r}, {n_layers} layers (anchor at 0), "
+                 f"rho={w.rho}",
+        "pool_us": round(1e3 * float(relay_t[:, 0].mean()), 2),
+        "pool_GBps": round(pool_bytes / (1e-3 * float(relay_t[:, 0].mean())) / 1e9, 1),
+        "pool_frac_hbm": round(pool_bytes / (1e-3 * float(relay_t[:, 0].mean())) / 1e9 / PEAK["hbm"], 4),
+        "route_us_anchor": round(1e3 * float(relay_t[0, 1]), 2),
+        "route_us_relay_median": round(1e3 * float(np.median(relay_t[relay_layers, 1])), 2) if relay_layers else None,
+        "route_us_full_median": round(1e3 * float(np.median(full_t[:, 1])), 2),
+        "attention_us_median": round(float(np.median(attn_us)), 1),
+        "attention_TFLOPs": round(float(np.median(attn_tflops)), 1),
+        "attention_frac_mfma_bf16": round(float(np.median(attn_tflops)) / PEAK["mfma_bf16"], 4),
+        "rerouted_frac_relay_layers": round(float(rer[1:].sum() / (len(relay_layers) * H * nc)), 4)
+        if relay_layers else None,
+        "layer_us_relay_median": round(1e3 * float(np.median(lt_relay[relay_layers])), 1) if relay_layers else None,
+        "layer_us_full_median": round(1e3 * float(np.median(lt_full[relay_layers])), 1) if relay_layers else None,
+        "routing_share_of_layer_full": round(float(np.median(full_t[:, 1] / lt_full)), 4),
+        "layer_speedup_vs_full": round(float(np.median(lt_full[relay_layers]) / np.median(lt_relay[relay_layers])), 4)
+        if relay_layers else None,
+    }
+
+
+def prefill_inputs(dev, layer=0):
+    """One layer of the prefill point's tokens with routes from full routing of
+    their pooled chunk representations (for counter passes)."""
+    import torch
+    from paper_2609_07306_amd import routerelay as rr
+    from paper_2609_07306_amd import synth
+    w = synth.preset("gqa", n_layers=layer + 1, anchor_every=0)
+    chunk, d, H, Hkv, nc = 256, w.d, w.n_heads, w.n_kv_heads, w.n
+    n = nc * chunk
+    lay = synth.layers(w)
+    g = torch.Generator(device=dev).manual_seed(1000 + layer)
+    sig = 0.5 / d ** 0.5
+    Qc0 = rr.to_device(lay[layer][2], "bf16", dev).float()
+    Kc0 = rr.to_device(lay[layer][3], "bf16", dev).float()
+    Q = (Qc0.repeat_interleave(chunk, 1) + sig * torch.randn((H, n, d), generator=g, device=dev)).to(torch.bfloat16)
+    K = (Kc0.repeat_interleave(chunk, 1) + sig * torch.randn((Hkv, n, d), generator=g, device=dev)).to(torch.bfloat16)
+    V = (torch.randn((Hkv, n, d), generator=g, device=dev) / d ** 0.5).to(torch.bfloat16)
+    Qc, Kc = rr.pool_chunks(Q, chunk), rr.pool_chunks(K, chunk)
+    routes = torch.empty((H * nc, w.k), dtype=torch.int32, device=dev)
+    rr.full_route(rr.Config(H, Hkv, nc, nc, d, w.k, 0, 0, "bf16", True), Qc, Kc, routes)
+    return {"Q": Q, "K": K, "V": V, "routes": routes, "chunk": chunk, "O": torch.empty_like(Q)}
+
+
 def study(args, dev):
     """Fidelity studies of the paper's Sec. 5 on this build's generator:
     the sentinel ablation (Sec. 5.2, Table 3 shape) and RouteRelay against a
@@ -487,6 +621,18 @@ def main():
 
     if args.study:
         print(json.dumps(study(args, dev)))
+        return
+    if args.counter_pass == "attention":
+        # the prefill shape's pooling (twice) and sparse attention (three times) on one layer
+        pf = prefill_inputs(dev)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            rr.sparse_attention(pf["Q"], pf["K"], pf["V"], pf["routes"], pf["chunk"], True, out=pf["O"])
+        torch.cuda.synchronize()
+        print(json.dumps({"counter_pass": "attention", "launches": 3}))
+        return
+    if args.prefill_only:
+        print(json.dumps({"prefill": prefill(dev, max(2, args.prefill_layers))}))
         return
 
     kw = {}
@@ -576,7 +722,7 @@ def main():
     }
     kernels = {}
     for kind, (tms, n) in prof.items():
-        if n == 0:
+        if n == 0 or kind not in alg:
             continue
         us = 1e3 * tms / n
         bound, amount, unit, peak = alg[kind]
@@ -682,6 +828,11 @@ def main():
         cb = dataclasses.replace(cfg, k_rows=torch.from_numpy(kr).to(dev))
         out["budgets"] = {"widths": sorted(set(kr.tolist())), "mean_width": round(float(kr.mean()), 3),
                           **operating_point(w, cb, dev, steps_op)}
+
+    # ---- the path inside a prefill: pooling, routing, sparse attention
+    if args.prefill_layers > 0:
+        out["prefill"] = prefill(dev, args.prefill_layers)
+        torch.cuda.empty_cache()
 
     # ---- measured peaks beside the nominal ones
     mp = measured_peaks(dev)

@@ -108,10 +108,12 @@ __global__ void expand_kernel(const int32_t *__restrict__ routes, int64_t rows, 
 // ------------------------------------------------------ sparse attention
 
 constexpr int kQT = 256;            // query tokens per workgroup
-constexpr int kAW = kQT / 32;       // waves
+constexpr int kQB = 1;              // 32-query blocks per wave (each K / V operand read feeds kQB products)
+constexpr int kAW = kQT / (32 * kQB);  // waves (one per SIMD)
 constexpr int kAT = 64 * kAW;       // threads
 constexpr int kKB = 64;             // keys per staged sub-block
 constexpr int kVRS = 2 * kKB + 16;  // bytes per row of the transposed V tile (dims x keys)
+constexpr float kLazy = 8.f;        // log2 headroom of the running softmax maximum
 
 template <int D>
 struct AttnShape {
@@ -259,26 +261,36 @@ __global__ __launch_bounds__(kAT) void sparse_attention_kernel(AttnArgs a)
         }
     };
 
-    const int t0 = q_lo + 32 * w;  // this wave's first query
+    const int t0 = q_lo + 32 * kQB * w;  // this wave's first query
     const bool wave_on = t0 < q_hi;
-    const int t = t0 + l32;
-    const bool q_ok = t < q_hi;
-    Frag<bf16_t, D> fq;
     const bf16_t *Qg = static_cast<const bf16_t *>(a.Q);
-    if (q_ok)
-        fq.load(Qg + ((int64_t)h * a.n_tokens + t) * D, hh);
-    else
-        fq.zero();
+    Frag<bf16_t, D> fq[kQB];
+#pragma unroll
+    for (int qb = 0; qb < kQB; ++qb) {
+        const int t = t0 + 32 * qb + l32;
+        if (t < q_hi)
+            fq[qb].load(Qg + ((int64_t)h * a.n_tokens + t) * D, hh);
+        else
+            fq[qb].zero();
+    }
     const float c2 = a.scale * 1.4426950408889634f;  // scores in log2 units
 
     constexpr int NMB = D / 32;
-    f32x16_t o[NMB];
+    f32x16_t o[kQB][NMB];
 #pragma unroll
-    for (int mb = 0; mb < NMB; ++mb) {
+    for (int qb = 0; qb < kQB; ++qb) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) o[mb][r] = 0.f;
+        for (int mb = 0; mb < NMB; ++mb) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) o[qb][mb][r] = 0.f;
+        }
     }
-    float m_run = -INFINITY, l_run = 0.f;
+    float m_run[kQB], l_run[kQB];
+#pragma unroll
+    for (int qb = 0; qb < kQB; ++qb) {
+        m_run[qb] = -INFINITY;
+        l_run[qb] = 0.f;
+    }
 
     const bf16_t *Kh = static_cast<const bf16_t *>(a.K) + (int64_t)g * a.n_tokens * D;
     const bf16_t *Vh = static_cast<const bf16_t *>(a.V) + (int64_t)g * a.n_tokens * D;
@@ -309,49 +321,74 @@ __global__ __launch_bounds__(kAT) void sparse_attention_kernel(AttnArgs a)
         for (int kb = 0; kb < kKB / 32; ++kb) {
             const int k0 = u0 + 32 * kb;
             // (wave-uniform) keys of this block exist and some reach a query of the wave
-            if (!wave_on || k0 >= u1 || (a.causal && k0 > t0 + 31)) continue;
-            f32x16_t s = {};
+            if (!wave_on || k0 >= u1 || (a.causal && k0 > t0 + 32 * kQB - 1)) continue;
+            // S^T = K Q^T for the wave's query blocks: each K operand feeds kQB products
+            f32x16_t sc[kQB];
+#pragma unroll
+            for (int qb = 0; qb < kQB; ++qb) sc[qb] = f32x16_t{};
 #pragma unroll
             for (int q = 0; q < D / 16; ++q) {
                 const bf16x8_t kf =
                     *reinterpret_cast<const bf16x8_t *>(buf + (32 * kb + l32) * S::KRS + hh * D + 16 * q);
-                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, fq.v[q], s, 0, 0, 0);
-            }
-            // mask, then the online-softmax update of this lane's query
-            float mx = -INFINITY;
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int u = k0 + acc_row(r, hh);
-                const bool ok = u < u1 && (!a.causal || u <= t);
-                s[r] = ok ? s[r] * c2 : -INFINITY;
-                mx = fmaxf(mx, s[r]);
+                for (int qb = 0; qb < kQB; ++qb)
+                    sc[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, fq[qb].v[q], sc[qb], 0, 0, 0);
             }
-            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-            const float m_new = fmaxf(m_run, mx);
-            const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-            const float alpha = exp2f(m_run - m_use);
-            float ls = 0.f;
-            bf16x8_t pb[2];
+            // (wave-uniform) no key of the block is masked for any query of the wave
+            const bool open = k0 + 31 < u1 && (!a.causal || k0 + 31 <= t0);
+            bf16x8_t pb[kQB][2];
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const float p = exp2f(s[r] - m_use);
-                ls += p;
-                pb[r >> 3][r & 7] = (__bf16)p;
+            for (int qb = 0; qb < kQB; ++qb) {
+                // mask, then the online-softmax update of this lane's query.  The
+                // running maximum m (in log2 units) moves only when a score
+                // exceeds it by more than kLazy, so the rescaling of O and l
+                // (one multiply per accumulator) is rare; weights are then at
+                // most 2^kLazy, and the normalised result is the same
+                if (!open) {  // (wave-uniform) key u is admissible iff u <= lim
+                    const int t = t0 + 32 * qb + l32;
+                    const int lim = a.causal ? min(u1 - 1, t) : u1 - 1;
+#pragma unroll
+                    for (int r = 0; r < 16; ++r)
+                        sc[qb][r] = (k0 + acc_row(r, hh) <= lim) ? sc[qb][r] : -INFINITY;
+                }
+                float mx = sc[qb][0];
+#pragma unroll
+                for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sc[qb][r]);
+                mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c2;
+                const bool bump = mx > m_run[qb] + kLazy;
+                if (__ballot(bump) != 0ull) {  // (wave-uniform) some query of the wave moves its maximum
+                    const float m_new = bump ? mx : m_run[qb];
+                    const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - m_new);  // 0 from -inf, 1 if unmoved
+                    l_run[qb] *= alpha;
+#pragma unroll
+                    for (int mb = 0; mb < NMB; ++mb) {
+#pragma unroll
+                        for (int r = 0; r < 16; ++r) o[qb][mb][r] *= alpha;
+                    }
+                    m_run[qb] = m_new;
+                }
+                const float m_use = (m_run[qb] == -INFINITY) ? 0.f : m_run[qb];
+                float ls = 0.f;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    // (v_exp_f32 flushes results below 2^-126 to zero: weights that small vanish
+                    // in the binary32 sums anyway)
+                    const float pr = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[qb][r], c2, -m_use));
+                    ls += pr;
+                    pb[qb][r >> 3][r & 7] = (__bf16)pr;
+                }
+                l_run[qb] += ls;
             }
-            l_run = l_run * alpha + ls;
-            m_run = m_new;
-#pragma unroll
-            for (int mb = 0; mb < NMB; ++mb) {
-#pragma unroll
-                for (int r = 0; r < 16; ++r) o[mb][r] *= alpha;
-            }
+            // O^T += V^T P^T: each V operand feeds kQB products
 #pragma unroll
             for (int mb = 0; mb < NMB; ++mb) {
 #pragma unroll
                 for (int s2 = 0; s2 < 2; ++s2) {
                     const bf16x8_t vf = *reinterpret_cast<const bf16x8_t *>(
                         vt + (32 * mb + l32) * kVRS + 2 * (32 * kb + 16 * s2 + 8 * hh));
-                    o[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[s2], o[mb], 0, 0, 0);
+#pragma unroll
+                    for (int qb = 0; qb < kQB; ++qb)
+                        o[qb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[qb][s2], o[qb][mb], 0, 0, 0);
                 }
             }
         }
@@ -360,21 +397,26 @@ __global__ __launch_bounds__(kAT) void sparse_attention_kernel(AttnArgs a)
         cur = nxt;
     }
 
-    // normalise and write this lane's query row (4 consecutive features per
-    // store); the two lane halves of a query hold the partial sums of l
-    const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
-    if (q_ok) {
-        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-        bf16_t *orow = static_cast<bf16_t *>(a.O) + ((int64_t)h * a.n_tokens + t) * D;
+    // normalise and write each query row (4 consecutive features per store);
+    // the two lane halves of a query hold the partial sums of l
 #pragma unroll
-        for (int mb = 0; mb < NMB; ++mb) {
+    for (int qb = 0; qb < kQB; ++qb) {
+        const int t = t0 + 32 * qb + l32;
+        const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32, 64);
+        if (t < q_hi) {
+            const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+            bf16_t *orow = static_cast<bf16_t *>(a.O) + ((int64_t)h * a.n_tokens + t) * D;
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int f = 32 * mb + 8 * q + 4 * hh;
-                uint2 pk;
-                pk.x = (uint32_t)float_to_bf16(o[mb][4 * q] * inv) | ((uint32_t)float_to_bf16(o[mb][4 * q + 1] * inv) << 16);
-                pk.y = (uint32_t)float_to_bf16(o[mb][4 * q + 2] * inv) | ((uint32_t)float_to_bf16(o[mb][4 * q + 3] * inv) << 16);
-                *reinterpret_cast<uint2 *>(orow + f) = pk;
+            for (int mb = 0; mb < NMB; ++mb) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int f = 32 * mb + 8 * q + 4 * hh;
+                    const f32x16_t &ov = o[qb][mb];
+                    uint2 pk;
+                    pk.x = (uint32_t)float_to_bf16(ov[4 * q] * inv) | ((uint32_t)float_to_bf16(ov[4 * q + 1] * inv) << 16);
+                    pk.y = (uint32_t)float_to_bf16(ov[4 * q + 2] * inv) | ((uint32_t)float_to_bf16(ov[4 * q + 3] * inv) << 16);
+                    *reinterpret_cast<uint2 *>(orow + f) = pk;
+                }
             }
         }
     }
