@@ -109,7 +109,7 @@ __global__ void expand_kernel(const int32_t *__restrict__ routes, int64_t rows, 
 
 constexpr int kQT = 256;            // query tokens per workgroup
 constexpr int kQB = 1;              // 32-query blocks per wave (each K / V operand read feeds kQB products)
-constexpr int kAW = kQT / (32 * kQB);  // waves (one per SIMD)
+constexpr int kAW = kQT / (32 * kQB);  // waves (two per SIMD)
 constexpr int kAT = 64 * kAW;       // threads
 constexpr int kKB = 64;             // keys per staged sub-block
 constexpr int kVRS = 2 * kKB + 16;  // bytes per row of the transposed V tile (dims x keys)
