@@ -517,6 +517,7 @@ def prefill(dev, n_layers, steps=2):
         "route_us_relay_median": round(1e3 * float(np.median(relay_t[relay_layers, 1])), 2) if relay_layers else None,
         "route_us_full_median": round(1e3 * float(np.median(full_t[:, 1])), 2),
         "attention_us_median": round(float(np.median(attn_us)), 1),
+        "attention_flop_layer0": float(4.0 * d * pairs[0]),
         "attention_TFLOPs": round(float(np.median(attn_tflops)), 1),
         "attention_frac_mfma_bf16": round(float(np.median(attn_tflops)) / PEAK["mfma_bf16"], 4),
         "rerouted_frac_relay_layers": round(float(rer[1:].sum() / (len(relay_layers) * H * nc)), 4)
