@@ -517,6 +517,7 @@ def prefill(dev, n_layers, steps=2):
         "route_us_relay_median": round(1e3 * float(np.median(relay_t[relay_layers, 1])), 2) if relay_layers else None,
         "route_us_full_median": round(1e3 * float(np.median(full_t[:, 1])), 2),
         "attention_us_median": round(float(np.median(attn_us)), 1),
+        "attention_queries_per_s": round(H * n / (1e-6 * float(np.median(attn_us))), 1),
         "attention_flop_layer0": float(4.0 * d * pairs[0]),
         "attention_TFLOPs": round(float(np.median(attn_tflops)), 1),
         "attention_frac_mfma_bf16": round(float(np.median(attn_tflops)) / PEAK["mfma_bf16"], 4),
@@ -527,7 +528,40 @@ def prefill(dev, n_layers, steps=2):
         "routing_share_of_layer_full": round(float(np.median(full_t[:, 1] / lt_full)), 4),
         "layer_speedup_vs_full": round(float(np.median(lt_full[relay_layers]) / np.median(lt_relay[relay_layers])), 4)
         if relay_layers else None,
+        "cpu_oracle": prefill_oracle_time(tokens(0), cfg, chunk, dev),
     }
+
+
+def prefill_oracle_time(toks, cfg, chunk, dev, n_queries=96):
+    """The binary64 oracle of pooling and sparse attention timed on this host
+    (one thread) on a sample of the prefill point's layer 0: pooling of query
+    head 0, and attention for n_queries query tokens of head 0 spread over the
+    sequence, along the library's full routes."""
+    import numpy as np
+    import torch
+    from oracle import consumer
+    from paper_2609_07306_amd import routerelay as rr
+    Q, K, V = toks
+    H, n, d = Q.shape
+    nc = n // chunk
+    Qc, Kc = rr.pool_chunks(Q, chunk), rr.pool_chunks(K, chunk)
+    routes = torch.empty((H * nc, cfg.k), dtype=torch.int32, device=dev)
+    rr.full_route(dataclasses.replace(cfg, m=0, r=0, relay="auto"), Qc, Kc, routes)
+    R = routes.cpu().numpy()
+    Q0 = Q[0:1].float().cpu().numpy()
+    K0, V0 = K[0:1].float().cpu().numpy(), V[0:1].float().cpu().numpy()
+    t0 = time.perf_counter()
+    consumer.pool_chunks(Q0, chunk)
+    t_pool = time.perf_counter() - t0
+    toks_q = [(0, int(t)) for t in np.linspace(0, n - 1, n_queries).astype(np.int64)]
+    t0 = time.perf_counter()
+    consumer.sparse_attention(Q0, K0, V0, R[:nc], chunk, True, rows=toks_q)
+    t_attn = time.perf_counter() - t0
+    return {"pool_tokens_per_s": round(n / t_pool, 1),
+            "attention_queries_per_s": round(n_queries / t_attn, 1),
+            "cores": 1, "kind": "oracle",
+            "sample": f"pooling of query head 0 ({n} tokens, {t_pool:.2f} s); attention for {n_queries} query "
+                      f"tokens of head 0 along full routes ({t_attn:.2f} s); numpy binary64, one thread"}
 
 
 def prefill_inputs(dev, layer=0):
