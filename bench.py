@@ -21,7 +21,12 @@ step, timed with HIP events the library records on its launch stream;
 this host's cores (``cpu_baseline_1thread``: one thread).  Also reported:
 per-layer near-tie counts, fidelity (recall, rerouted fraction, score pairs)
 averaged over seeds 0, 1, 2, the low-drift operating points of the same
-shape, and measured copy and GEMM rates beside the nominal peaks.
+shape, per-row route budgets and sentinel / trigger variants on the same
+shape, the path inside a prefill (pooling, routing and sparse attention on
+the causal GQA prefill shape, with the oracle timed beside it), and measured
+copy and GEMM rates beside the nominal peaks.  ``--study`` runs the fidelity
+studies instead; ``--counter-pass`` and ``--copy-calibration`` are programs
+for rocprofv3 counter passes.
 """
 from __future__ import annotations
 
@@ -93,6 +98,8 @@ def parse():
     ap.add_argument("--budgets", default="quarters",
                     help="per-row route widths of the budgets point: 'quarters' (k/4, k/2, 3k/4, k), "
                          "a comma list, or '' for none")
+    ap.add_argument("--variants", default="2,2,1",
+                    help="sentinel / trigger variant point: n_sink,n_recent,min_reuse ('' for none)")
     ap.add_argument("--prefill-layers", type=int, default=8,
                     help="layers of the prefill point (pooling + routing + sparse attention on the causal GQA "
                          "prefill shape); 0 for none")
@@ -863,6 +870,15 @@ def main():
         cb = dataclasses.replace(cfg, k_rows=torch.from_numpy(kr).to(dev))
         out["budgets"] = {"widths": sorted(set(kr.tolist())), "mean_width": round(float(kr.mean()), 3),
                           **operating_point(w, cb, dev, steps_op)}
+
+    # ---- sentinel and trigger variants: mandatory sink / recent sentinels and
+    # the minimum reuse horizon on the same workload
+    if args.variants:
+        ns, nr, mr = (int(x) for x in args.variants.split(","))
+        wv = w.with_(n_sink=ns, n_recent=nr, min_reuse=mr)
+        print(f"[bench] variants n_sink={ns} n_recent={nr} min_reuse={mr}", file=sys.stderr, flush=True)
+        cv = dataclasses.replace(rr.Config.of(wv), relay=args.relay)
+        out["variants"] = {"n_sink": ns, "n_recent": nr, "min_reuse": mr, **operating_point(wv, cv, dev, steps_op)}
 
     # ---- the path inside a prefill: pooling, routing, sparse attention
     if args.prefill_layers > 0:
