@@ -98,7 +98,7 @@ def parse():
     ap.add_argument("--budgets", default="quarters",
                     help="per-row route widths of the budgets point: 'quarters' (k/4, k/2, 3k/4, k), "
                          "a comma list, or '' for none")
-    ap.add_argument("--variants", default="2,2,1",
+    ap.add_argument("--variants", default="2,2,0",
                     help="sentinel / trigger variant point: n_sink,n_recent,min_reuse ('' for none)")
     ap.add_argument("--prefill-layers", type=int, default=8,
                     help="layers of the prefill point (pooling + routing + sparse attention on the causal GQA "
