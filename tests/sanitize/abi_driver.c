@@ -113,6 +113,26 @@ int main(void)
     EXPECT(rr_set_sweep_cap(0) == RR_OK);
     EXPECT(rr_unconverged_rows(NULL) == RR_ERR_INVALID);
 
+    /* either side of the path: argument checks refuse these before any
+     * launch (the pointers are never dereferenced) */
+    void *fake = (void *)0x1000;
+    EXPECT(rr_pool_chunks(NULL, 1, 64, 128, 8, RR_BF16, fake, NULL) == RR_ERR_INVALID);
+    EXPECT(rr_pool_chunks(fake, 1, 64, 12, 8, RR_BF16, fake, NULL) == RR_ERR_INVALID);
+    EXPECT(rr_pool_chunks(fake, 1, 64, 128, 0, RR_BF16, fake, NULL) == RR_ERR_INVALID);
+    EXPECT(rr_expand_tokens(NULL, 1, 4, 8, 64, (int32_t *)fake, NULL) == RR_ERR_INVALID);
+    EXPECT(rr_expand_tokens((const int32_t *)fake, 1, 70000, 70000, 64, (int32_t *)fake, NULL) == RR_ERR_INVALID);
+    rr_attn_config ac;
+    memset(&ac, 0, sizeof(ac));
+    ac.n_heads = 4; ac.n_kv_heads = 2; ac.n_tokens = 512; ac.d = 128; ac.chunk = 64; ac.k = 4;
+    ac.causal = 1; ac.dtype = RR_BF16;
+    EXPECT(rr_sparse_attention(NULL, fake, fake, fake, (const int32_t *)fake, fake, NULL) == RR_ERR_INVALID);
+    ac.d = 96;
+    EXPECT(rr_sparse_attention(&ac, fake, fake, fake, (const int32_t *)fake, fake, NULL) == RR_ERR_UNSUPPORTED);
+    ac.d = 128; ac.k = 300;
+    EXPECT(rr_sparse_attention(&ac, fake, fake, fake, (const int32_t *)fake, fake, NULL) == RR_ERR_INVALID);
+    ac.k = 4; ac.scale = NAN;
+    EXPECT(rr_sparse_attention(&ac, fake, fake, fake, (const int32_t *)fake, fake, NULL) == RR_ERR_INVALID);
+
     /* a valid configuration: allocation fails cleanly without a GPU, or
      * succeeds and is released */
     c = base();

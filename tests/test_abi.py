@@ -177,3 +177,47 @@ def test_sweep_cap_hook_validates():
     assert rr.lib.rr_set_sweep_cap(-1) == -1
     assert rr.lib.rr_set_sweep_cap(0) == 0
     assert rr.lib.rr_unconverged_rows(None) == -1
+
+
+def test_attention_config_layout():
+    rr = _rr()
+    assert ctypes.sizeof(rr._AttnConfig) == 40
+    assert rr._AttnConfig.scale.offset == 32 and rr._AttnConfig.reserved.offset == 36
+
+
+def _attn_cfg(rr, **kw):
+    base = dict(n_heads=4, n_kv_heads=2, n_tokens=512, d=128, chunk=64, k=4, causal=1, dtype=rr.RR_BF16,
+                scale=0.0, reserved=0)
+    base.update(kw)
+    return rr._AttnConfig(*base.values())
+
+
+# pointers that are never dereferenced: every call below is refused by the
+# host-side checks before any launch
+FAKE = ctypes.c_void_p(0x1000)
+
+
+@pytest.mark.parametrize("kw,status", [
+    ({"n_heads": 3}, -1), ({"n_tokens": 0}, -1), ({"chunk": 0}, -1), ({"k": 0}, -1), ({"k": 257}, -1),
+    ({"causal": 2}, -1), ({"reserved": 1}, -1), ({"scale": -1.0}, -1), ({"scale": float("inf")}, -1),
+    ({"dtype": 7}, -1), ({"dtype": 0}, -5), ({"d": 96}, -5), ({"d": 256}, -5),
+])
+def test_sparse_attention_rejects_bad_configs(kw, status):
+    rr = _rr()
+    c = _attn_cfg(rr, **kw)
+    assert rr.lib.rr_sparse_attention(ctypes.byref(c), FAKE, FAKE, FAKE, FAKE, FAKE, None) == status
+
+
+def test_consumer_calls_reject_null_and_bad_sizes():
+    rr = _rr()
+    c = _attn_cfg(rr)
+    assert rr.lib.rr_sparse_attention(None, FAKE, FAKE, FAKE, FAKE, FAKE, None) == -1
+    assert rr.lib.rr_sparse_attention(ctypes.byref(c), FAKE, None, FAKE, FAKE, FAKE, None) == -1
+    assert rr.lib.rr_pool_chunks(None, 1, 64, 128, 8, rr.RR_BF16, FAKE, None) == -1
+    for h, n, d, ch, dt in ((0, 64, 128, 8, 1), (1, 0, 128, 8, 1), (1, 64, 12, 8, 1), (1, 64, 2048, 8, 1),
+                            (1, 64, 128, 0, 1), (1, 64, 128, 8, 5)):
+        assert rr.lib.rr_pool_chunks(FAKE, h, n, d, ch, dt, FAKE, None) == -1
+    assert rr.lib.rr_expand_tokens(None, 1, 4, 8, 64, FAKE, None) == -1
+    for rows, k, ch, n in ((0, 4, 8, 64), (1, 0, 8, 64), (1, 4, 0, 64), (1, 4, 8, 0), (1, 70000, 70000, 64)):
+        assert rr.lib.rr_expand_tokens(FAKE, rows, k, ch, n, FAKE, None) == -1
+    assert b"" != rr.lib.rr_last_error()
