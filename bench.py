@@ -595,7 +595,7 @@ def prefill_inputs(dev, layer=0):
 
 
 def study(args, dev):
-    """Fidelity studies of the paper's Sec. 5 on this build's generator:
+    """Fidelity studies of the paper's Sec. 5 on the synthetic generator:
     the sentinel ablation (Sec. 5.2, Table 3 shape) and RouteRelay against a
     fixed refresh stride (Sec. 5.1, Table 2 shape); means over seeds."""
     import numpy as np

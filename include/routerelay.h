@@ -50,7 +50,7 @@ typedef enum {
     RR_ERR_OOM = -2,         /* device allocation failed */
     RR_ERR_HIP = -3,         /* a HIP runtime call failed (message in rr_last_error) */
     RR_ERR_STATE = -4,       /* call order violated (relay before any anchor, layer going back) */
-    RR_ERR_UNSUPPORTED = -5  /* valid but outside the shapes this build supports */
+    RR_ERR_UNSUPPORTED = -5  /* valid but outside the shapes the library supports */
 } rr_status;
 
 typedef enum { RR_F32 = 0, RR_BF16 = 1 } rr_dtype;
