@@ -145,7 +145,7 @@ struct Stage {
         const u32x4_t z = {0u, 0u, 0u, 0u};
 #pragma unroll
         for (int q = 0; q < S::KPT; ++q) {
-            const int it = tid + q * kAT, key = it & (kKB - 1), grp = it / kKB;
+            const int it = tid + q * kAT, grp = it % (D / 8), key = it / (D / 8);  // consecutive lanes: one row
             const bool ok = it < S::KITEMS && u0 + key < u1;
             k[q] = ok ? *reinterpret_cast<const u32x4_t *>(Kh + (int64_t)(u0 + key) * D + 8 * grp) : z;
         }
@@ -164,7 +164,7 @@ struct Stage {
         using S = AttnShape<D>;
 #pragma unroll
         for (int q = 0; q < S::KPT; ++q) {
-            const int it = tid + q * kAT, key = it & (kKB - 1), grp = it / kKB;
+            const int it = tid + q * kAT, grp = it % (D / 8), key = it / (D / 8);  // consecutive lanes: one row
             if (it < S::KITEMS) *reinterpret_cast<u32x4_t *>(buf + key * S::KRS + 16 * grp) = k[q];
         }
         unsigned char *vt = buf + S::KBYTES;
