@@ -112,74 +112,63 @@ constexpr int kQB = 1;              // 32-query blocks per wave (each K / V oper
 constexpr int kAW = kQT / (32 * kQB);  // waves (two per SIMD)
 constexpr int kAT = 64 * kAW;       // threads
 constexpr int kKB = 64;             // keys per staged sub-block
-constexpr int kVRS = 2 * kKB + 16;  // bytes per row of the transposed V tile (dims x keys)
 constexpr float kLazy = 8.f;        // log2 headroom of the running softmax maximum
 
 template <int D>
 struct AttnShape {
     static constexpr int KRS = 2 * D + 16;           // bytes per row of the K tile
+    // bytes per row of the V tile: the transposed reads of 16 lanes cover 4
+    // rows x 32 bytes, which this stride places in distinct banks for the 32
+    // lanes served together
+    static constexpr int VRS = 2 * D + 64;
     static constexpr int KBYTES = kKB * KRS;          // K tile
-    static constexpr int VBYTES = D * kVRS;           // transposed V tile
+    static constexpr int VBYTES = kKB * VRS;          // V tile (row-major like K)
     static constexpr int BUF = KBYTES + VBYTES;       // one stage
     static constexpr int LDS = 2 * BUF;               // double-buffered
-    static constexpr int KITEMS = kKB * (D / 8);      // 16-byte K pieces per sub-block
-    static constexpr int VITEMS = (kKB / 2) * (D / 8);  // (key pair, 8 features) V pieces
-    static constexpr int KPT = (KITEMS + kAT - 1) / kAT;
-    static constexpr int VPT = (VITEMS + kAT - 1) / kAT;
+    static constexpr int ITEMS = kKB * (D / 8);       // 16-byte pieces of K (and of V) per sub-block
+    static constexpr int PT = (ITEMS + kAT - 1) / kAT;
 };
 
-// Position of key x (0..63) of a sub-block in the transposed V tile: bits 2
-// and 3 swapped, the order in which a lane half holds keys in the S^T
-// accumulator (rows 8*(i>>2) + 4*hh + (i&3) of register i).
-__device__ __forceinline__ int vpos(int x) { return (x & ~12) | ((x & 4) << 1) | ((x & 8) >> 1); }
+typedef short short4_t __attribute__((ext_vector_type(4)));
 
-// One sub-block's staging registers: its K pieces and V key-pair pieces.
+// Four bf16 of a transposed LDS read (ds_read_b64_tr_b16): lane i of each
+// 16-lane group receives element i % 4 of the 8 bytes that lane 4e + i / 4 of
+// its group addresses, as element e.
+__device__ __forceinline__ short4_t lds_read_tr16(const unsigned char *p)
+{
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) short4_t *)p);
+}
+
+// One sub-block's staging registers: its K and V pieces (consecutive lanes
+// read one key row).
 template <int D>
 struct Stage {
-    u32x4_t k[AttnShape<D>::KPT];
-    u32x4_t v0[AttnShape<D>::VPT], v1[AttnShape<D>::VPT];
+    u32x4_t k[AttnShape<D>::PT], v[AttnShape<D>::PT];
 
     __device__ __forceinline__ void load(const bf16_t *Kh, const bf16_t *Vh, int u0, int u1, int tid)
     {
         using S = AttnShape<D>;
         const u32x4_t z = {0u, 0u, 0u, 0u};
 #pragma unroll
-        for (int q = 0; q < S::KPT; ++q) {
-            const int it = tid + q * kAT, grp = it % (D / 8), key = it / (D / 8);  // consecutive lanes: one row
-            const bool ok = it < S::KITEMS && u0 + key < u1;
-            k[q] = ok ? *reinterpret_cast<const u32x4_t *>(Kh + (int64_t)(u0 + key) * D + 8 * grp) : z;
-        }
-#pragma unroll
-        for (int q = 0; q < S::VPT; ++q) {
-            const int it = tid + q * kAT, p = it & (kKB / 2 - 1), grp = it / (kKB / 2);
-            const bool in = it < S::VITEMS;
-            const int a = u0 + 2 * p, b = a + 1;
-            v0[q] = (in && a < u1) ? *reinterpret_cast<const u32x4_t *>(Vh + (int64_t)a * D + 8 * grp) : z;
-            v1[q] = (in && b < u1) ? *reinterpret_cast<const u32x4_t *>(Vh + (int64_t)b * D + 8 * grp) : z;
+        for (int q = 0; q < S::PT; ++q) {
+            const int it = tid + q * kAT, grp = it % (D / 8), key = it / (D / 8);
+            const bool ok = it < S::ITEMS && u0 + key < u1;
+            const int64_t off = (int64_t)(u0 + key) * D + 8 * grp;
+            k[q] = ok ? *reinterpret_cast<const u32x4_t *>(Kh + off) : z;
+            v[q] = ok ? *reinterpret_cast<const u32x4_t *>(Vh + off) : z;
         }
     }
 
     __device__ __forceinline__ void store(unsigned char *buf, int tid) const
     {
         using S = AttnShape<D>;
-#pragma unroll
-        for (int q = 0; q < S::KPT; ++q) {
-            const int it = tid + q * kAT, grp = it % (D / 8), key = it / (D / 8);  // consecutive lanes: one row
-            if (it < S::KITEMS) *reinterpret_cast<u32x4_t *>(buf + key * S::KRS + 16 * grp) = k[q];
-        }
         unsigned char *vt = buf + S::KBYTES;
 #pragma unroll
-        for (int q = 0; q < S::VPT; ++q) {
-            const int it = tid + q * kAT, p = it & (kKB / 2 - 1), grp = it / (kKB / 2);
-            if (it < S::VITEMS) {
-                const int col = 2 * vpos(2 * p);  // byte offset of the pair (keys 2p, 2p+1 stay adjacent)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    // features 8*grp + 2e and 8*grp + 2e + 1 of the two keys
-                    const uint32_t a = v0[q][e], b = v1[q][e];
-                    *reinterpret_cast<uint32_t *>(vt + (8 * grp + 2 * e) * kVRS + col) = (a & 0xFFFFu) | (b << 16);
-                    *reinterpret_cast<uint32_t *>(vt + (8 * grp + 2 * e + 1) * kVRS + col) = (a >> 16) | (b & 0xFFFF0000u);
-                }
+        for (int q = 0; q < S::PT; ++q) {
+            const int it = tid + q * kAT, grp = it % (D / 8), key = it / (D / 8);
+            if (it < S::ITEMS) {
+                *reinterpret_cast<u32x4_t *>(buf + key * S::KRS + 16 * grp) = k[q];
+                *reinterpret_cast<u32x4_t *>(vt + key * S::VRS + 16 * grp) = v[q];
             }
         }
     }
@@ -384,8 +373,18 @@ __global__ __launch_bounds__(kAT) void sparse_attention_kernel(AttnArgs a)
             for (int mb = 0; mb < NMB; ++mb) {
 #pragma unroll
                 for (int s2 = 0; s2 < 2; ++s2) {
-                    const bf16x8_t vf = *reinterpret_cast<const bf16x8_t *>(
-                        vt + (32 * mb + l32) * kVRS + 2 * (32 * kb + 16 * s2 + 8 * hh));
+                    // the A operand of lane (feature 32 mb + l32, half hh): keys
+                    // k0 .. k0+3 and k0+8 .. k0+11 of the block, k0 = 16 s2 + 4 hh,
+                    // the order in which the accumulator holds this half's keys
+                    // (rows 8*(i>>2) + 4*hh + (i&3) of register i); two transposed
+                    // reads, lane j of each 16-lane group addressing key row
+                    // k0 + j/4 at features 16*(l32/16) + 4*(j%4) of the block
+                    const int j = lane & 15;
+                    const unsigned char *vp = vt + (32 * kb + 16 * s2 + 4 * hh + (j >> 2)) * S::VRS +
+                                              2 * (32 * mb + 16 * (l32 >> 4) + 4 * (j & 3));
+                    const short4_t lo = lds_read_tr16(vp), hi = lds_read_tr16(vp + 8 * S::VRS);
+                    const bf16x8_t vf = __builtin_bit_cast(
+                        bf16x8_t, (short __attribute__((ext_vector_type(8)))){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
 #pragma unroll
                     for (int qb = 0; qb < kQB; ++qb)
                         o[qb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[qb][s2], o[qb][mb], 0, 0, 0);
