@@ -289,3 +289,88 @@ def rollout_subset(w, heads, layers, relay="auto", note=print):
         note(f"  layer {layer}: compared {int(trusted.sum())} of {len(rows)} rows")
     L.close()
     return stats
+
+
+def step_compare(w, heads=None, relay="auto", k_rows=None, gamma_rows=None, note=print):
+    """Step mode: before each relay layer the oracle's ledger is imported into
+    the GPU ledger (on the rows compared; the GPU keeps its own state on the
+    others), so both sides start every layer from the same state and each
+    layer is compared on its own near-ties only (T1 / T2 of that layer, T3 of
+    that relay), with no taint carried between layers.  heads: the query
+    heads whose rows the oracle computes (None: all).  Anchors are compared
+    the same way.  Returns per-layer statistics."""
+    p = problem_of(w)
+    cfg = dataclasses.replace(rr.Config.of(w), relay=relay)
+    device = torch.device("cuda", torch.cuda.current_device())
+    if k_rows is not None:
+        k32 = np.ascontiguousarray(k_rows, dtype=np.int32)
+        p = dataclasses.replace(p, k_rows=k32)
+        cfg = dataclasses.replace(cfg, k_rows=torch.from_numpy(k32).to(device))
+    if gamma_rows is not None:
+        g32 = np.ascontiguousarray(gamma_rows, dtype=np.float32)
+        p = dataclasses.replace(p, gamma_rows=g32.astype(np.float64))
+        cfg = dataclasses.replace(cfg, gamma_rows=torch.from_numpy(g32).to(device))
+    heads = list(range(p.n_heads)) if heads is None else list(heads)
+    head_rows = [np.arange(h * p.n_q, (h + 1) * p.n_q, dtype=np.int64) for h in heads]
+    rows = np.concatenate(head_rows)
+    ni = n_valid_rows(p)[rows]
+    gam = (p.gamma_rows[rows] if p.gamma_rows is not None else np.full(len(rows), p.gamma))
+    L = rr.Ledger(cfg)
+    ref = oracle.new_ledger(p)
+    mask_t = torch.empty(p.rows, dtype=torch.uint8, device=device)
+    pairs_t = torch.zeros(1, dtype=torch.int64, device=device)
+    stats = {"layers": 0, "rows": 0, "compared": 0, "mask_compared": 0, "rerouted": 0}
+    for layer, Qf, Kf, Qd, Kd in synth.Generator(w):
+        Q, K = dev(Qd, w.dtype), dev(Kd, w.dtype)
+        bounds = np.concatenate(_oracle_threads(lambda r: oracle.route_bounds(p, Qf, Kf, r), p, head_rows))
+        t1 = gap_tie(bounds[:, 0], bounds[:, 1], bounds[:, 4], bounds[:, 5], p.d)
+        t2 = gap_tie(bounds[:, 2], bounds[:, 3], bounds[:, 6], bounds[:, 7], p.d)
+        if w.is_anchor(layer):
+            L.anchor(layer, Q, K)
+            _oracle_threads(lambda r: oracle.anchor(p, layer, Qf, Kf, ref, rows=r), p, head_rows)
+            trusted = ~(t1 | t2)
+            omask = np.ones(len(rows), dtype=bool)
+        else:
+            # both sides start the layer from the oracle's state
+            cur = ledger_np(L)
+            for key in ("routes", "sent", "build", "age"):
+                cur[key][rows] = ref[key][rows]
+            imp = {k: torch.from_numpy(np.ascontiguousarray(v)).to(device) for k, v in cur.items()}
+            L.import_(layer - 1, imp["routes"], imp["sent"] if p.sent_width else None, imp["build"], imp["age"])
+            L.relay(layer, Q, K, mask=mask_t, pairs=pairs_t)
+            outs = _oracle_threads(lambda r: oracle.relay(p, layer, Qf, Kf, ref, rows=r), p, head_rows)
+            out = {k: np.concatenate([o[k][r] for o, r in zip(outs, head_rows)])
+                   for k in ("mask", "row_pairs", "alpha", "beta", "alpha_abs", "beta_abs")}
+            gmask = mask_t.cpu().numpy().astype(bool)[rows]
+            omask = out["mask"].astype(bool)
+            with np.errstate(invalid="ignore"):
+                diff = np.where(np.isfinite(gam), np.abs(out["alpha"] - (out["beta"] + gam)), np.inf)
+                t3 = np.nan_to_num(diff, nan=np.inf) < tau(out["alpha"], out["beta"], out["alpha_abs"],
+                                                          out["beta_abs"], p.d)
+            decided = ~t3
+            bad = np.flatnonzero(decided & (gmask != omask))
+            assert len(bad) == 0, f"step layer {layer}: mask differs on rows {rows[bad[:8]]}"
+            sent_rows = cur["sent"][rows] if p.sent_width else np.zeros((len(rows), 0), np.int32)
+            cand = (cur["routes"][rows] >= 0).sum(1) + (sent_rows >= 0).sum(1)
+            gpu_row_pairs = cand + gmask.astype(np.int64) * ni
+            bad = np.flatnonzero(decided & (gpu_row_pairs != out["row_pairs"]))
+            assert len(bad) == 0, f"step layer {layer}: score pairs differ on rows {rows[bad[:8]]}"
+            trusted = decided & ~(omask & (t1 | t2))
+            alpha, beta, _ = L.relay_stats()
+            torch.cuda.synchronize()
+            alpha, beta = alpha.cpu().numpy()[rows], beta.cpu().numpy()[rows]
+            score_check(alpha, out["alpha"], out["alpha_abs"], p.d, w.dtype, stats)
+            score_check(beta, out["beta"], out["beta_abs"], p.d, w.dtype, stats)
+            stats["mask_compared"] += int(decided.sum())
+            stats["rerouted"] += int(gmask.sum())
+        got = ledger_np(L)
+        for key in ("routes", "sent", "build", "age"):
+            a, b = got[key][rows][trusted], ref[key][rows][trusted]
+            assert np.array_equal(a, b), f"step layer {layer}: {key} differs on rows " \
+                f"{rows[np.flatnonzero((a != b).reshape(len(a), -1).any(1))[:8]]}"
+        stats["layers"] += 1
+        stats["rows"] += len(rows)
+        stats["compared"] += int(trusted.sum())
+        note(f"  step layer {layer}: compared {int(trusted.sum())} of {len(rows)} rows")
+    L.close()
+    return stats

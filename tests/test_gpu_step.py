@@ -1,0 +1,82 @@
+"""Step-mode parity: before every relay layer the oracle's ledger is imported
+into the GPU ledger (rr_ledger_import), so each layer is compared from the
+same state on its own near-ties only -- no taint is carried across layers, so
+nearly every row is compared at every layer, at small sizes and at the full
+sizes of the benchmark's workloads (oracle on a head subset)."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_07306_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    torch.cuda.set_device(0)
+    yield
+
+
+def note(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+STEP_CASES = [
+    ("drift", {"n_heads": 4, "n_kv_heads": 4, "n_layers": 6, "rho": 0.3}, 0.95),
+    ("gqa", {"n_heads": 8, "n_kv_heads": 2, "n": 256, "n_layers": 6}, 0.95),
+    ("longctx", {"n_heads": 2, "n_kv_heads": 2, "n": 512, "n_layers": 5}, 0.6),
+    ("tiny", {"m": 0, "r": 6, "n_layers": 5}, 0.95),
+    ("tiny", {"m": 6, "r": 0, "n_layers": 5, "causal": True}, 0.95),
+    ("gqa", {"n_heads": 8, "n_kv_heads": 2, "n": 256, "n_layers": 5, "n_sink": 2, "n_recent": 3, "min_reuse": 1}, 0.95),
+    # dense rescoring tiles and the compacted reroute
+    ("scale", {"n_heads": 256, "n_kv_heads": 256, "n": 128, "n_layers": 4, "anchor_every": 2}, 0.95),
+]
+
+
+@pytest.mark.parametrize("relay", ["split", "one_pass"])
+@pytest.mark.parametrize("name,kw,floor", STEP_CASES, ids=[f"{n}-{i}" for i, (n, _, _) in enumerate(STEP_CASES)])
+def test_step_parity(name, kw, floor, relay):
+    from parity_util import step_compare
+    w = synth.preset(name, **kw)
+    note(f"step mode {name} {kw} ({relay})")
+    st = step_compare(w, relay=relay, note=note)
+    note(f"  {st}")
+    assert st["compared"] >= floor * st["rows"]
+    assert st["rerouted"] > 0
+
+
+def test_step_parity_budgets_and_margins():
+    from parity_util import step_compare
+    w = synth.preset("drift", n_heads=4, n_kv_heads=4, n_layers=5, rho=0.2)
+    kr = synth.route_budgets(w)
+    g = np.random.default_rng(4).choice(np.array([0.0, 0.02, np.inf, -np.inf], np.float32), size=w.rows)
+    note("step mode with per-row widths and margins")
+    st = step_compare(w, k_rows=kr, gamma_rows=g, note=note)
+    note(f"  {st}")
+    assert st["compared"] >= 0.95 * st["rows"] and st["rerouted"] > 0
+
+
+FULL_STEP = [
+    # the benchmark's headline workload: anchor, seven relays, anchor
+    ("scale", {"n": 1024, "n_layers": 9}, [0, 17], 0.97),
+    # the causal GQA shape over a whole anchor period
+    ("gqa", {"n_layers": 9}, [0, 5, 30], 0.97),
+    # long context with crowded top-k boundaries (duplicated keys)
+    ("longctx", {"n_layers": 3}, [7], 0.9),
+]
+
+
+@pytest.mark.parametrize("name,kw,heads,floor", FULL_STEP, ids=[n for n, _, _, _ in FULL_STEP])
+def test_step_parity_full_size(name, kw, heads, floor):
+    from parity_util import step_compare
+    w = synth.preset(name, **kw)
+    note(f"full-size step mode {name} {kw}, oracle heads {heads}")
+    st = step_compare(w, heads=heads, note=note)
+    note(f"  {st}")
+    assert st["compared"] >= floor * st["rows"]
