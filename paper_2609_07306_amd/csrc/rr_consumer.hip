@@ -8,15 +8,15 @@
 //
 // Sparse attention.  A workgroup takes up to 256 query tokens of one query
 // chunk (8 waves of 32 queries, one head) and walks the route of that chunk:
-// each routed chunk is cut into 64-key sub-blocks, staged in LDS (K row-major;
-// V transposed, so that a lane's MFMA operand is one 16-byte read) with the
-// next sub-block's global loads in flight during the current one's products.
-// Per 32-key block a wave computes S^T = K Q^T (keys x queries, so every lane
-// owns one query), applies the mask and the online-softmax update in
-// registers, and accumulates O^T = V^T P^T with P taken straight from the
-// S^T accumulator: the keys of the PV product are ordered the way the
-// accumulator holds them (bits 2 and 3 of the key index swapped within each
-// 16-key group), and the transposed V tile is written in that order.
+// each routed chunk is cut into 64-key sub-blocks, staged in LDS (K and V
+// row-major, loaded a key row per 16 lanes) with the next sub-block's global
+// loads in flight during the current one's products.  Per 32-key block a
+// wave computes S^T = K Q^T (keys x queries, so every lane owns one query),
+// applies the mask and the online-softmax update in registers, and
+// accumulates O^T = V^T P^T with P taken straight from the S^T accumulator:
+// the keys of the PV product are ordered the way the accumulator holds them
+// (each lane half holds groups of 4 consecutive keys, 8 apart), and the V^T
+// operand is read from the row-major V tile with the LDS transpose read.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
