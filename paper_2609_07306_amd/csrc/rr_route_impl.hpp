@@ -1,13 +1,17 @@
 // Row-wise GEMM + TopK routing for gfx950 (RouteRelay, arXiv 2609.07306).
 //
-// One kernel serves three callers:
+// One kernel serves four callers:
 //   MODE_FULL    -- full routing of every row, Eq. (1)-(2) (the baseline);
 //   MODE_ANCHOR  -- full routing plus the ledger build of Sec. 3.1: the
 //                   chunks ranked k+1..k+m become near-miss sentinels and r
 //                   random sentinels are drawn from what is left;
 //   MODE_REROUTE -- the same for the rows a relay layer flagged (Sec. 3.2,
 //                   row-selective refresh of Sec. 4.2), read per head from
-//                   the flag array in ascending row order.
+//                   the flag array in ascending row order;
+//   MODE_RELAY   -- the one-pass relay: the threshold sweep also rescores
+//                   each row's ledger (Eq. (5)-(7)) from per-row bitmaps,
+//                   the trigger of Eq. (8) flags the row, and the tile's
+//                   flagged rows are routed as in MODE_REROUTE.
 //
 // A workgroup owns a tile of 32*NW query rows of one head and runs KS waves
 // per 32-row block: the KS waves of a block split the key range between them
@@ -43,17 +47,23 @@
 //      is pinned (bisection bounds adjacent) the id cut of its ties is found
 //      by a second bisection, so that exactly T chunks are admitted.  Repairs
 //      change work, never results.
-// Selection is lane-serial: a bitonic sorting network in registers over the
-// first NET candidates, plus insertion of any further ones, gives the k-th
-// and T-th scores, and one pass over the id-ordered candidates assigns R and
-// the near-miss set (equal scores rank the lower id first) and writes both
-// sorted by id.  The random sentinels are drawn by the same lane: a pool of
-// at most half the valid chunks by rank (the y-th free chunk of a per-row
-// bitmap of R, N and earlier draws), a larger one by counter-hash probes
-// reduced modulo n_i (Barrett), rejected with the bitmap (exact up to 4096
-// chunks where the row's candidate region holds 128 words, else 2048; beyond
-// that a filter on the id modulo the bitmap's width whose hits are checked by
-// binary search of R and N and a scan of the earlier draws).
+// Selection runs on four lanes per row (lanes l, l+16, l+32, l+48 of a
+// wave, every wave of the workgroup): a bitonic network over the first NET
+// candidates, sorted in quarters and merged across the row's lanes, plus
+// insertion of any further ones, gives the k-th and T-th scores; each lane
+// then assigns R and the near-miss set over a quarter of the id-ordered
+// candidates (equal scores rank the lower id first), writing both sorted by
+// id at offsets from the counts of the quarters before it.  The random
+// sentinels are drawn by the same four lanes: a pool of at most half the
+// valid chunks by rank (the y-th free chunk of a per-row bitmap of R, N and
+// earlier draws), a larger one by counter-hash probes reduced modulo n_i
+// (Barrett), rejected with the bitmap (exact up to 4096 chunks where the
+// row's candidate region holds 128 words, else 2048; beyond that a filter
+// on the id modulo the bitmap's width whose hits are checked by binary
+// search of R and N and a scan of the earlier draws).  Slots whose outcome
+// depends only on their own hash (first probes, rank draws' ranks) are
+// hashed four at a time and decided in slot order, so the draws are those of
+// one lane deciding the slots one by one.
 //
 // This header holds the kernel template; each rr_route_<type>_<mode>.hip
 // translation unit instantiates one input type and caller, so the library
