@@ -673,11 +673,29 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
     if (a.pairs_out && (mode == MODE_FULL || mode == MODE_ANCHOR) && blockIdx.x == 0 && tid == 0)
         *a.pairs_out = a.pairs_value;
 
-    // Reroute: the per-head tile table (heads in XCD-major order) from the
-    // rescoring workgroups' flagged-row counts; workgroup 0 also publishes the
-    // call's totals (rerouted rows, score pairs).
+    // Reroute.  With a workgroup for every tile that full routing would have
+    // (the grid covers them all), workgroup b owns full routing's tile (h, t)
+    // and needs only its head's flagged-row count (rows of ranks [t BM,
+    // (t+1) BM) among the head's flagged rows, if any).  Otherwise the
+    // workgroups share a per-head tile table (heads in XCD-major order) built
+    // from the rescoring workgroups' flagged-row counts.  Workgroup 0 also
+    // publishes the call's totals (rerouted rows, score pairs).
     int32_t *tb = reinterpret_cast<int32_t *>(smem + a.lds_tiles);
-    if (mode == MODE_REROUTE) {
+    const int max_tiles = a.n_heads * a.tiles_per_head;
+    const bool own_tile = mode == MODE_REROUTE && (int)gridDim.x >= max_tiles;
+    __shared__ int32_t s_hcount;
+    if (mode == MODE_REROUTE && own_tile) {
+        if (w == 0 && (int)blockIdx.x < max_tiles) {
+            int hb, tb0;
+            tile_of_block(blockIdx.x, a.n_heads, a.n_kv_heads, a.tiles_per_head, hb, tb0);
+            const int32_t *bc = a.blk_count + (int64_t)hb * a.rescore_bph;
+            int c = 0;
+            for (int b = lane; b < a.rescore_bph; b += 64) c += bc[b];
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off, 64);
+            if (lane == 0) s_hcount = c;
+        }
+    } else if (mode == MODE_REROUTE) {
         for (int j = tid; j < a.n_heads; j += C::NT) {
             const int hd = head_at(j, a.n_heads, a.n_kv_heads);
             const int32_t *bc = a.blk_count + (int64_t)hd * a.rescore_bph;
@@ -693,6 +711,8 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
             for (; b < a.rescore_bph; ++b) c += bc[b];
             tb[j + 1] = (c + BM - 1) / BM;
         }
+    }
+    if (mode == MODE_REROUTE) {
         if (blockIdx.x == 0) {
             if (tid == 0) {
                 s_tot_pairs = 0ull;
@@ -717,7 +737,7 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
             }
         }
         __syncthreads();
-        if (w == 0) {
+        if (w == 0 && !own_tile) {
             // inclusive scan of the heads' tile counts, 64 heads at a time
             int carry = 0;
             for (int j0 = 0; j0 < a.n_heads; j0 += 64) {
@@ -742,11 +762,22 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
         __syncthreads();
     }
 
-    // Tiles of this workgroup.  Full / anchor: one tile per workgroup, mapped
-    // XCD-aware.  Reroute: the XCD's contiguous range of the tile table
-    // (heads in XCD-major order), strided over the XCD's workgroups.
+    // Tiles of this workgroup.  Full / anchor, and reroute with a workgroup
+    // per possible tile: one tile per workgroup, mapped XCD-aware.  Other
+    // reroutes: the XCD's contiguous range of the tile table (heads in
+    // XCD-major order), strided over the XCD's workgroups.
     int tile, t_end, t_step;
-    if (mode == MODE_REROUTE) {
+    if (mode == MODE_REROUTE && own_tile) {
+        tile = blockIdx.x;
+        t_step = gridDim.x;
+        int ok = 0;
+        if (tile < max_tiles) {
+            int hb, tb0;
+            tile_of_block(tile, a.n_heads, a.n_kv_heads, a.tiles_per_head, hb, tb0);
+            ok = tb0 * BM < s_hcount;
+        }
+        t_end = ok ? tile + 1 : tile;
+    } else if (mode == MODE_REROUTE) {
         if ((a.n_kv_heads & 7) == 0 && (gridDim.x & 7) == 0) {
             const int x = blockIdx.x & 7, hx = a.n_heads >> 3;
             tile = tb[x * hx] + (int)(blockIdx.x >> 3);
@@ -773,7 +804,7 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
         const int rb = w % NW, p = w / NW;
         // ---------------------------------------------------- rows of the tile
         int h, t;
-        if (mode == MODE_REROUTE) {
+        if (mode == MODE_REROUTE && !own_tile) {
             if (tid == 0) s_head = 0;
             __syncthreads();
             for (int j = tid; j < a.n_heads; j += C::NT)
