@@ -51,13 +51,17 @@ struct DenseEpi {
     const uint2 *bmr;  // this lane's row: (R word, C word) per 32 keys
     int nrow;          // SEED: valid keys of the lane's row (0: padding row)
     float top[SEED ? 16 : 1][2];
+    uint2 wnext;       // this stage's words, read a stage ahead (set to stage 0's
+                       // before the sweep; the row's bitmap has a word past the
+                       // last stage's)
 
     template <class F>
     __device__ __forceinline__ void step(int st, const f32x16_t &acc, f32x16_t &next, const F &fq, const F &fk,
                                          bool full)
     {
         const int k0 = sbase + 16 * st;  // this lane's keys: k0 .. k0 + 15 (k0 % 16 == 0)
-        const uint2 wv = bmr[k0 >> 5];
+        const uint2 wv = wnext;
+        wnext = bmr[(k0 + 16) >> 5];
         next = route_detail::tile_product(fq, fk);
         const uint32_t sh = (uint32_t)(k0 & 16);
         const uint32_t mr = wv.x >> sh, mc = wv.y >> sh;
@@ -208,6 +212,7 @@ __global__ __launch_bounds__(128 * NW) void rescore_dense_kernel(RescoreArgs a)
     epi.bmax = -INFINITY;
     epi.sbase = myseg * seg;
     epi.bmr = bm + myrow * nwd;
+    epi.wnext = epi.bmr[epi.sbase >> 5];
     epi.nrow = nrow;
     if constexpr (SEED) {
 #pragma unroll

@@ -467,13 +467,17 @@ struct RelayEpi {
     int sbase;  // first key of the lane's segment
     float amin, bmax;
     const uint2 *bmr;  // this lane's row bitmap
+    uint2 wnext;       // this stage's words, read a stage ahead (set to stage 0's
+                       // before the sweep; the row's bitmap has a word past the
+                       // last stage's)
 
     template <class F>
     __device__ __forceinline__ void step(int st, const f32x16_t &acc, f32x16_t &next, const F &fq, const F &fk,
                                          bool full)
     {
         const int k0 = sbase + 16 * st;  // this lane's keys: k0 .. k0 + 15 (k0 % 16 == 0)
-        const uint2 wv = bmr[k0 >> 5];
+        const uint2 wv = wnext;
+        wnext = bmr[(k0 + 16) >> 5];
         next = tile_product(fq, fk);
         const uint32_t sh = (uint32_t)(k0 & 16);
         const uint32_t mr = wv.x >> sh, mc = wv.y >> sh;
@@ -993,6 +997,7 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
                 epi.amin = INFINITY;
                 epi.bmax = -INFINITY;
                 epi.bmr = rbm + myrow * a.bm_words;
+                epi.wnext = epi.bmr[sbase >> 5];
                 sweep_keys<DT, D, C>(fq, Kg, a.n_k, seg, nb, full_stages, tid, p, hh, l32, bt, epi);
                 // the row's lanes: halves hh of a wave here, key splits p below
                 const float am = fminf(epi.amin, __shfl_xor(epi.amin, 32, 64));
