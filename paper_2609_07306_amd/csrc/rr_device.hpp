@@ -99,10 +99,13 @@ __device__ __forceinline__ uint64_t sm64(uint64_t z)
     return z ^ (z >> 31);
 }
 
+// (The next three are host functions as well, so that a host program can
+// check them against exact integer arithmetic.)
+//
 // x mod m for 0 < m < 2^16, exactly the 64-bit remainder: long division in
 // 16-bit digits, where each partial remainder (< m) times 2^16 plus the next
 // digit stays below 2^32, so four 32-bit remainders replace the 64-bit one.
-__device__ __forceinline__ uint32_t mod_u64_small(uint64_t x, uint32_t m)
+__host__ __device__ __forceinline__ uint32_t mod_u64_small(uint64_t x, uint32_t m)
 {
     uint32_t r = (uint32_t)(x >> 48) % m;
     r = ((r << 16) | (uint32_t)((x >> 32) & 0xffffu)) % m;
@@ -111,7 +114,7 @@ __device__ __forceinline__ uint32_t mod_u64_small(uint64_t x, uint32_t m)
 }
 
 // floor((2^64 - 1) / m) for 0 < m < 2^16, by the same 16-bit long division
-__device__ __forceinline__ uint64_t max_u64_div_small(uint32_t m)
+__host__ __device__ __forceinline__ uint64_t max_u64_div_small(uint32_t m)
 {
     uint64_t q = 0;
     uint32_t r = 0;
@@ -126,13 +129,13 @@ __device__ __forceinline__ uint64_t max_u64_div_small(uint32_t m)
 
 // Position of the y-th (0-based) set bit of z, for y < popc(z): a binary
 // search on the population counts of the lower halves.
-__device__ __forceinline__ int select_bit(uint32_t z, int y)
+__host__ __device__ __forceinline__ int select_bit(uint32_t z, int y)
 {
     int pos = 0;
 #pragma unroll
     for (int wdt = 16; wdt > 0; wdt >>= 1) {
         const uint32_t lo = z & ((1u << wdt) - 1u);
-        const int c = __popc(lo);
+        const int c = __builtin_popcount(lo);
         const bool up = y >= c;
         y = up ? y - c : y;
         z = up ? (z >> wdt) : lo;
