@@ -127,6 +127,19 @@ __host__ __device__ __forceinline__ uint64_t max_u64_div_small(uint32_t m)
     return q;
 }
 
+// Largest v over the wave's active lanes, for 0 <= v < 2^nbits, wave-uniform:
+// the bits of the maximum from the top, one ballot each.  (An atomic max from
+// every lane compiles to a loop over the active lanes, one at a time.)
+__device__ __forceinline__ int wave_max_small(int v, int nbits)
+{
+    int m = 0;
+    for (int b = nbits - 1; b >= 0; --b) {
+        const int c = m | (1 << b);
+        m = (__ballot(v >= c) != 0ull) ? c : m;
+    }
+    return m;
+}
+
 // Position of the y-th (0-based) set bit of z, for y < popc(z): a binary
 // search on the population counts of the lower halves.
 __host__ __device__ __forceinline__ int select_bit(uint32_t z, int y)

@@ -878,13 +878,18 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
             }
         }
         __syncthreads();
-        if (tid < BM && row_g[tid] >= 0) {
-            const int i = row_i[tid];
-            row_n[tid] = a.causal ? min(i + 1, a.n_k) : a.n_k;
-            // the row's route width k_i (Sec. 4.3): it selects T_i = k_i + m
-            // chunks; the threshold bounds of T = k + m >= T_i stay valid
-            row_k[tid] = a.k_rows ? min(max(a.k_rows[row_g[tid]], 1), a.k) : a.k;
-            atomicMax(&s_ncols, row_n[tid]);
+        if (tid < BM) {  // whole waves (BM is 32, or a multiple of 64)
+            int rn = 0;
+            if (row_g[tid] >= 0) {
+                const int i = row_i[tid];
+                rn = a.causal ? min(i + 1, a.n_k) : a.n_k;
+                row_n[tid] = rn;
+                // the row's route width k_i (Sec. 4.3): it selects T_i = k_i + m
+                // chunks; the threshold bounds of T = k + m >= T_i stay valid
+                row_k[tid] = a.k_rows ? min(max(a.k_rows[row_g[tid]], 1), a.k) : a.k;
+            }
+            const int m = wave_max_small(rn, 32 - __clz(a.n_k));
+            if (lane == 0 && m > 0) atomicMax(&s_ncols, m);
         }
         __syncthreads();
         const int ncols = s_ncols;
