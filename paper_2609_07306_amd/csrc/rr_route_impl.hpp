@@ -678,28 +678,16 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
         *a.pairs_out = a.pairs_value;
 
     // Reroute.  With a workgroup for every tile that full routing would have
-    // (the grid covers them all), workgroup b owns full routing's tile (h, t)
-    // and needs only its head's flagged-row count (rows of ranks [t BM,
-    // (t+1) BM) among the head's flagged rows, if any).  Otherwise the
+    // (the grid covers them all), workgroup b owns full routing's tile (h, t):
+    // its rows are the head's flagged rows of ranks [t BM, (t+1) BM), found by
+    // the flag ranking below (none: the tile is skipped).  Otherwise the
     // workgroups share a per-head tile table (heads in XCD-major order) built
-    // from the rescoring workgroups' flagged-row counts.  Workgroup 0 also
-    // publishes the call's totals (rerouted rows, score pairs).
+    // from the rescoring workgroups' flagged-row counts.  Wave 0 of workgroup 0
+    // also publishes the call's totals (rerouted rows, score pairs).
     int32_t *tb = reinterpret_cast<int32_t *>(smem + a.lds_tiles);
     const int max_tiles = a.n_heads * a.tiles_per_head;
     const bool own_tile = mode == MODE_REROUTE && (int)gridDim.x >= max_tiles;
-    __shared__ int32_t s_hcount;
-    if (mode == MODE_REROUTE && own_tile) {
-        if (w == 0 && (int)blockIdx.x < max_tiles) {
-            int hb, tb0;
-            tile_of_block(blockIdx.x, a.n_heads, a.n_kv_heads, a.tiles_per_head, hb, tb0);
-            const int32_t *bc = a.blk_count + (int64_t)hb * a.rescore_bph;
-            int c = 0;
-            for (int b = lane; b < a.rescore_bph; b += 64) c += bc[b];
-#pragma unroll
-            for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off, 64);
-            if (lane == 0) s_hcount = c;
-        }
-    } else if (mode == MODE_REROUTE) {
+    if (mode == MODE_REROUTE && !own_tile) {
         for (int j = tid; j < a.n_heads; j += C::NT) {
             const int hd = head_at(j, a.n_heads, a.n_kv_heads);
             const int32_t *bc = a.blk_count + (int64_t)hd * a.rescore_bph;
@@ -717,16 +705,28 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
         }
     }
     if (mode == MODE_REROUTE) {
-        if (blockIdx.x == 0) {
-            if (tid == 0) {
-                s_tot_pairs = 0ull;
-                s_tot_rows = 0;
-            }
-            __syncthreads();
+        if (blockIdx.x == 0 && w == 0) {
+            // register sums over the rescoring workgroups' counts, four loads
+            // of each kind in flight per lane
             unsigned long long pp = 0;
             int cc = 0;
             const int nb = a.n_heads * a.rescore_bph;
-            for (int j = tid; j < nb; j += C::NT) {
+            int j = lane;
+            for (; j + 192 < nb; j += 256) {
+                int64_t p4[4];
+                int c4[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    p4[u] = a.blk_pairs[j + 64 * u];
+                    c4[u] = a.blk_count[j + 64 * u];
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    pp += (unsigned long long)p4[u];
+                    cc += c4[u];
+                }
+            }
+            for (; j < nb; j += 64) {
                 pp += (unsigned long long)a.blk_pairs[j];
                 cc += a.blk_count[j];
             }
@@ -736,34 +736,32 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
                 cc += __shfl_xor(cc, off, 64);
             }
             if (lane == 0) {
-                atomicAdd(&s_tot_pairs, pp);
-                atomicAdd(&s_tot_rows, cc);
+                *a.stat_pairs = (int64_t)pp;
+                *a.stat_nrr = cc;
+                if (a.pairs_out) *a.pairs_out = (int64_t)pp;
+                if (a.nrr_out) *a.nrr_out = cc;
             }
         }
-        __syncthreads();
-        if (w == 0 && !own_tile) {
-            // inclusive scan of the heads' tile counts, 64 heads at a time
-            int carry = 0;
-            for (int j0 = 0; j0 < a.n_heads; j0 += 64) {
-                const int j = j0 + lane;
-                int v = (j < a.n_heads) ? tb[j + 1] : 0;
+        if (!own_tile) {
+            __syncthreads();
+            if (w == 0) {
+                // inclusive scan of the heads' tile counts, 64 heads at a time
+                int carry = 0;
+                for (int j0 = 0; j0 < a.n_heads; j0 += 64) {
+                    const int j = j0 + lane;
+                    int v = (j < a.n_heads) ? tb[j + 1] : 0;
 #pragma unroll
-                for (int off = 1; off < 64; off <<= 1) {
-                    const int u = __shfl_up(v, off, 64);
-                    v += (lane >= off) ? u : 0;
+                    for (int off = 1; off < 64; off <<= 1) {
+                        const int u = __shfl_up(v, off, 64);
+                        v += (lane >= off) ? u : 0;
+                    }
+                    if (j < a.n_heads) tb[j + 1] = v + carry;
+                    carry += __shfl(v, 63, 64);
                 }
-                if (j < a.n_heads) tb[j + 1] = v + carry;
-                carry += __shfl(v, 63, 64);
+                if (lane == 0) tb[0] = 0;
             }
-            if (lane == 0) tb[0] = 0;
+            __syncthreads();
         }
-        if (tid == 0 && blockIdx.x == 0) {
-            *a.stat_pairs = (int64_t)s_tot_pairs;
-            *a.stat_nrr = s_tot_rows;
-            if (a.pairs_out) *a.pairs_out = (int64_t)s_tot_pairs;
-            if (a.nrr_out) *a.nrr_out = s_tot_rows;
-        }
-        __syncthreads();
     }
 
     // Tiles of this workgroup.  Full / anchor, and reroute with a workgroup
@@ -774,13 +772,7 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
     if (mode == MODE_REROUTE && own_tile) {
         tile = blockIdx.x;
         t_step = gridDim.x;
-        int ok = 0;
-        if (tile < max_tiles) {
-            int hb, tb0;
-            tile_of_block(tile, a.n_heads, a.n_kv_heads, a.tiles_per_head, hb, tb0);
-            ok = tb0 * BM < s_hcount;
-        }
-        t_end = ok ? tile + 1 : tile;
+        t_end = tile < max_tiles ? tile + 1 : tile;
     } else if (mode == MODE_REROUTE) {
         if ((a.n_kv_heads & 7) == 0 && (gridDim.x & 7) == 0) {
             const int x = blockIdx.x & 7, hx = a.n_heads >> 3;
@@ -971,8 +963,13 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
         else
             fq.zero();
 
+        // the collection sweep's key ring; its first two stages are requested
+        // as soon as no other sweep needs the loads, so that they arrive
+        // during the threshold seeds or the threshold bound
+        u32x4_t breg[2][C::PER_T];
         // ------------------------------------------------ sweep 1: thresholds
         if (mode == MODE_REROUTE && a.seed_bound) {
+            sweep_db_first<C>(breg, Kg, a.n_k, seg, nb, tid);
             // the rescoring pass scored every key of these rows and left each
             // row's bound and maximum; they are widened by kSeedSlack orders
             // so that they hold even if its scores differ from this tile's in
@@ -1015,6 +1012,7 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
                 store_kept<C, TT>(us, myrow, myseg, epi.top);
             }
             __syncthreads();
+            sweep_db_first<C>(breg, Kg, a.n_k, seg, nb, tid);
             bound_of_kept<C>(us, tid, T, b1_s, rmax_s);
         } else {
             {
@@ -1031,6 +1029,7 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
                 store_kept<C, TT>(us, myrow, myseg, epi.top);
             }
             __syncthreads();
+            sweep_db_first<C>(breg, Kg, a.n_k, seg, nb, tid);
             bound_of_kept<C>(us, tid, T, b1_s, rmax_s);
         }
         __syncthreads();
@@ -1156,8 +1155,7 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
                 epi.dum = CAPR - off;
                 epi.ls = lsA + off;
                 epi.li = liA + off;
-                u32x4_t breg[2][C::PER_T];
-                sweep_db_first<C>(breg, Kg, a.n_k, seg, nb, tid);
+                if (it > 0) sweep_db_first<C>(breg, Kg, a.n_k, seg, nb, tid);
                 sweep_keys_db<DT, D, C>(fq, Kg, a.n_k, seg, nb, full_stages, tid, p, hh, l32, bt, breg, epi);
                 if (rstate[myrow] != kDone) seg_cnt[myseg][myrow] = epi.cnt;
             }
