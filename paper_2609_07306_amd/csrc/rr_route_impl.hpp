@@ -812,6 +812,15 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
         } else {
             tile_of_block(tile, a.n_heads, a.n_kv_heads, a.tiles_per_head, h, t);
         }
+        // reroute: the flags of the ranking's first pass are requested before
+        // the row set-up's barrier
+        const uint8_t *fl = a.flags + (int64_t)h * a.n_q;
+        bool fpre[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int i = 4 * tid + j;
+            fpre[j] = (mode == MODE_REROUTE) && (i < a.n_q) && fl[i] != 0;
+        }
         if (tid < BM) {
             row_g[tid] = -1;
             row_i[tid] = 0;
@@ -821,7 +830,6 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
         __syncthreads();
         if (mode == MODE_REROUTE) {
             const int lo = t * BM, hi = lo + BM;
-            const uint8_t *fl = a.flags + (int64_t)h * a.n_q;
             int run = 0;
             // thread tid takes rows base + 4 tid + j, j < 4 (the four loads in
             // flight together); ranks follow the row order
@@ -833,7 +841,7 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     const int i = base + 4 * tid + j;
-                    f[j] = (i < a.n_q) && fl[i] != 0;
+                    f[j] = (base == 0) ? fpre[j] : ((i < a.n_q) && fl[i] != 0);
                 }
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
@@ -860,16 +868,18 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
                     rank += f[j] ? 1 : 0;
                 }
                 run += tot;
-                __syncthreads();
+                __syncthreads();  // (also orders the rows' writes before their reads below)
             }
-        } else if (tid < BM) {
-            const int i = t * BM + tid;
-            if (i < a.n_q) {
-                row_i[tid] = i;
-                row_g[tid] = h * a.n_q + i;
+        } else {
+            if (tid < BM) {
+                const int i = t * BM + tid;
+                if (i < a.n_q) {
+                    row_i[tid] = i;
+                    row_g[tid] = h * a.n_q + i;
+                }
             }
+            __syncthreads();
         }
-        __syncthreads();
         if (tid < BM) {  // whole waves (BM is 32, or a multiple of 64)
             int rn = 0;
             if (row_g[tid] >= 0) {
