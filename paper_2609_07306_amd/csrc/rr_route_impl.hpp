@@ -1524,44 +1524,48 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
         // consecutive in memory except in reroute mode, where each row is
         // still one contiguous run) and marks R u N in the per-row bitmaps.
         // Thread tid visits (r, j) = divmod(tid + i * NT, width), stepped
-        // without divisions.
+        // without divisions, four visits at a time: the four rows' indices
+        // and staged ids are read from LDS before any of their stores.
         uint32_t *bw = reinterpret_cast<uint32_t *>(ss);
-        {
-            const int wd = a.k, dr = C::NT / wd, dj = C::NT - dr * wd;
+        auto copy_out = [&](int wd, int col0, auto &&put) __attribute__((always_inline)) {
+            const int dr = C::NT / wd, dj = C::NT - dr * wd;
             int r = tid / wd, j = tid - r * wd;
-            for (; r < BM; r += dr, j += dj) {
-                if (j >= wd) {
-                    j -= wd;
-                    ++r;
-                    if (r >= BM) break;
-                }
-                const int64_t g = row_g[r];
-                const int32_t id = stg[r * STG + j];
-                if (g >= 0) {
-                    if (a.led_routes) a.led_routes[g * a.k + j] = id;
-                    if (a.routes_out) a.routes_out[g * a.k + j] = id;
-                    if (mode != MODE_FULL && id >= 0)
-                        atomicOr(&bw[r * C::SS + ((id >> 5) & (C::BMW - 1))], 1u << (id & 31));
-                }
-            }
-        }
-        if (mode != MODE_FULL) {
-            if (a.m > 0) {
-                const int wd = a.m, dr = C::NT / wd, dj = C::NT - dr * wd;
-                int r = tid / wd, j = tid - r * wd;
-                for (; r < BM; r += dr, j += dj) {
+            while (r < BM) {
+                int rr[4], jj[4], gv[4], iv[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    rr[u] = r;
+                    jj[u] = j;
+                    r += dr;
+                    j += dj;
                     if (j >= wd) {
                         j -= wd;
                         ++r;
-                        if (r >= BM) break;
-                    }
-                    const int64_t g = row_g[r];
-                    const int32_t id = stg[r * STG + a.k + j];
-                    if (g >= 0) {
-                        a.led_sent[g * c_sent + j] = id;
-                        if (id >= 0) atomicOr(&bw[r * C::SS + ((id >> 5) & (C::BMW - 1))], 1u << (id & 31));
                     }
                 }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int rc = min(rr[u], BM - 1);  // (visits past the tile read its last row, unused)
+                    gv[u] = row_g[rc];
+                    iv[u] = stg[rc * STG + col0 + jj[u]];
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    if ((rr[u] < BM) & (gv[u] >= 0)) put(rr[u], jj[u], (int64_t)gv[u], iv[u]);
+            }
+        };
+        copy_out(a.k, 0, [&](int r, int j, int64_t g, int32_t id) __attribute__((always_inline)) {
+            if (a.led_routes) a.led_routes[g * a.k + j] = id;
+            if (a.routes_out) a.routes_out[g * a.k + j] = id;
+            if (mode != MODE_FULL && id >= 0)
+                atomicOr(&bw[r * C::SS + ((id >> 5) & (C::BMW - 1))], 1u << (id & 31));
+        });
+        if (mode != MODE_FULL) {
+            if (a.m > 0) {
+                copy_out(a.m, a.k, [&](int r, int j, int64_t g, int32_t id) __attribute__((always_inline)) {
+                    a.led_sent[g * c_sent + j] = id;
+                    if (id >= 0) atomicOr(&bw[r * C::SS + ((id >> 5) & (C::BMW - 1))], 1u << (id & 31));
+                });
             }
             for (int i = tid; i < BM; i += C::NT) {
                 const int64_t g = row_g[i];
