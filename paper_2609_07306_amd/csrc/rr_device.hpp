@@ -127,6 +127,14 @@ __host__ __device__ __forceinline__ uint64_t max_u64_div_small(uint32_t m)
     return q;
 }
 
+// x of lane (lane ^ 1), resp. (lane ^ 2), within each group of four lanes:
+// DPP quad permutations [1,0,3,2] and [2,3,0,1] (a VALU move, where a shuffle
+// through ds_bpermute takes an LDS round trip).  Every lane must be active.
+__device__ __forceinline__ int quad_xor1(int x) { return __builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, false); }
+__device__ __forceinline__ int quad_xor2(int x) { return __builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, false); }
+__device__ __forceinline__ float quad_xor1(float x) { return __int_as_float(quad_xor1(__float_as_int(x))); }
+__device__ __forceinline__ float quad_xor2(float x) { return __int_as_float(quad_xor2(__float_as_int(x))); }
+
 // Largest v over the wave's active lanes, for 0 <= v < 2^nbits, wave-uniform:
 // the bits of the maximum from the top, one ballot each.  (An atomic max from
 // every lane compiles to a loop over the active lanes, one at a time.)

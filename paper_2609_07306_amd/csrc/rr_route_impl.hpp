@@ -547,12 +547,14 @@ __device__ __forceinline__ void bound_of_kept(const float *us, int tid, int T, f
         umin = fminf(umin, fin ? u[q] : INFINITY);
         nfin += fin ? 1 : 0;
     }
-#pragma unroll
-    for (int off = 1; off < C::LPR; off <<= 1) {
-        rmax = fmaxf(rmax, __shfl_xor(rmax, off, 64));
-        umin = fminf(umin, __shfl_xor(umin, off, 64));
-        nfin += __shfl_xor(nfin, off, 64);
-    }
+    // a row's four lanes are a DPP quad
+    static_assert(C::LPR == 4 && C::NT % 64 == 0, "four bound lanes per row, whole waves");
+    rmax = fmaxf(rmax, quad_xor1(rmax));
+    umin = fminf(umin, quad_xor1(umin));
+    nfin += quad_xor1(nfin);
+    rmax = fmaxf(rmax, quad_xor2(rmax));
+    umin = fminf(umin, quad_xor2(umin));
+    nfin += quad_xor2(nfin);
     float lo = (nfin >= T) ? umin : -INFINITY, hi = rmax;
     if (lo > -INFINITY) {
         for (int it = 0; it < kBisect; ++it) {
@@ -564,8 +566,8 @@ __device__ __forceinline__ void bound_of_kept(const float *us, int tid, int T, f
 #pragma unroll
             for (int q = 0; q < C::UPL; ++q) neg += (int)(__float_as_uint(u[q] - mid) >> 31);
             int cnt = C::UPL - neg;
-#pragma unroll
-            for (int off = 1; off < C::LPR; off <<= 1) cnt += __shfl_xor(cnt, off, 64);
+            cnt += quad_xor1(cnt);
+            cnt += quad_xor2(cnt);
             if (cnt >= T)
                 lo = mid;
             else
