@@ -135,6 +135,46 @@ __device__ __forceinline__ int quad_xor2(int x) { return __builtin_amdgcn_update
 __device__ __forceinline__ float quad_xor1(float x) { return __int_as_float(quad_xor1(__float_as_int(x))); }
 __device__ __forceinline__ float quad_xor2(float x) { return __int_as_float(quad_xor2(__float_as_int(x))); }
 
+// Exchanges among the four lanes l16 + 16 q (q = 0..3, l16 = lane & 15) of a
+// wave, by gfx950's row swaps.  With both operands x, v_permlane16_swap
+// yields x of lanes l & ~16 and l | 16, v_permlane32_swap x of lanes l & ~32
+// and l | 32.  A lane's partners (its lane ^ 16, lane ^ 32) must be active.
+// Each swap costs two copies (it overwrites both operands), a wait state and
+// a select: it shortens a chain of dependent exchanges, where a shuffle
+// through ds_bpermute waits an LDS round trip each time, but many
+// independent exchanges pipeline better as shuffles.
+__device__ __forceinline__ void rows4(uint32_t x, uint32_t (&n)[4])
+{
+    const auto p = __builtin_amdgcn_permlane16_swap(x, x, false, false);        // x[l & ~16], x[l | 16]
+    const auto a = __builtin_amdgcn_permlane32_swap(p[0], p[0], false, false);  // x[l16], x[l16 + 32]
+    const auto b = __builtin_amdgcn_permlane32_swap(p[1], p[1], false, false);  // x[l16 + 16], x[l16 + 48]
+    n[0] = a[0];
+    n[1] = b[0];
+    n[2] = a[1];
+    n[3] = b[1];
+}
+// x of lane l16 + 16 q, for q the same in the four lanes
+__device__ __forceinline__ uint32_t from_row(uint32_t x, int q)
+{
+    const auto p = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    const uint32_t h = (q & 1) ? p[1] : p[0];
+    const auto a = __builtin_amdgcn_permlane32_swap(h, h, false, false);
+    return (q & 2) ? a[1] : a[0];
+}
+__device__ __forceinline__ float from_row(float x, int q) { return __uint_as_float(from_row(__float_as_uint(x), q)); }
+__device__ __forceinline__ uint32_t xor16(uint32_t x, int lane)
+{
+    const auto p = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    return (lane & 16) ? p[0] : p[1];
+}
+__device__ __forceinline__ uint32_t xor32(uint32_t x, int lane)
+{
+    const auto p = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+    return (lane & 32) ? p[0] : p[1];
+}
+__device__ __forceinline__ int xor16(int x, int lane) { return (int)xor16((uint32_t)x, lane); }
+__device__ __forceinline__ int xor32(int x, int lane) { return (int)xor32((uint32_t)x, lane); }
+
 // Largest v over the wave's active lanes, for 0 <= v < 2^nbits, wave-uniform:
 // the bits of the maximum from the top, one ballot each.  (An atomic max from
 // every lane compiles to a loop over the active lanes, one at a time.)

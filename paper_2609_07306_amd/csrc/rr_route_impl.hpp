@@ -1341,7 +1341,8 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
                 sort_desc<QN>(v);
                 // a bitonic split with the partner lane (lane ^ xm) of two
                 // descending runs, one taken reversed (rev) or both in place;
-                // the upper side keeps the larger of each pair
+                // the upper side keeps the larger of each pair (sixteen
+                // independent exchanges: LDS shuffles, which pipeline)
                 auto split = [&](int xm, bool upper, bool rev) __attribute__((always_inline)) {
                     if (rev) {
 #pragma unroll
@@ -1385,16 +1386,19 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
                 auto at_pos = [&](int g) {
                     const int gq = min(max(g, 0) / QN, 3);
                     const float x = sorted_at<QN>(v, min(max(g - qq * QN, 0), QN - 1));
-                    return __shfl(x, l16 + 16 * gq, 64);
+                    return from_row(x, gq);  // (g, hence gq, is the same in the row's lanes)
                 };
+                // (sum, prefix and position exchanges are dependent chains:
+                // row swaps, no LDS round trips)
                 auto sum4 = [&](int n) {
-                    n += __shfl_xor(n, 16, 64);
-                    return n + __shfl_xor(n, 32, 64);
+                    n += xor16(n, lane);
+                    return n + xor32(n, lane);
                 };
                 // exclusive prefix over the quarters
                 auto before = [&](int n) {
-                    const int n0 = __shfl(n, l16, 64), n1 = __shfl(n, l16 + 16, 64), n2 = __shfl(n, l16 + 32, 64);
-                    return (qq > 0 ? n0 : 0) + (qq > 1 ? n1 : 0) + (qq > 2 ? n2 : 0);
+                    uint32_t nq[4];
+                    rows4((uint32_t)n, nq);
+                    return (qq > 0 ? (int)nq[0] : 0) + (qq > 1 ? (int)nq[1] : 0) + (qq > 2 ? (int)nq[2] : 0);
                 };
                 const float vk = at_pos(ke - 1), vT = at_pos(Te - 1);
                 const int gtk = sum4(count_gt<QN>(v, vk)), gtT = sum4(count_gt<QN>(v, vT));
