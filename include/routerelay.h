@@ -70,13 +70,11 @@ typedef enum { RR_F32 = 0, RR_BF16 = 1 } rr_dtype;
  *     fit its LDS: n_k up to about 2048, d = 256 up to about 1900);
  *   split -- rescoring and trigger, then the routing of the flagged rows
  *     compacted per head (Sec. 4.2).
- * By default the one pass runs where it fits, except for non-causal inputs
- * whose rescoring uses dense tiles (n_k <= 2048 with enough tiles): there the
- * split schedule, whose reroute starts from the rescoring pass's threshold,
- * was measured faster.  (For causal inputs compaction would mix short and
- * long rows in one tile.)  RR_OPT_SPLIT_RELAY forces the split schedule,
- * RR_OPT_ONE_PASS_RELAY the one pass (RR_ERR_UNSUPPORTED where it does not
- * fit); not both. */
+ * By default causal inputs take the one pass where it fits (compaction would
+ * mix short and long causal rows in one tile) and other inputs the split
+ * schedule, measured faster for them.  RR_OPT_SPLIT_RELAY forces the split
+ * schedule, RR_OPT_ONE_PASS_RELAY the one pass (RR_ERR_UNSUPPORTED where it
+ * does not fit); not both. */
 typedef enum { RR_OPT_SPLIT_RELAY = 1, RR_OPT_ONE_PASS_RELAY = 2 } rr_option;
 
 typedef struct {

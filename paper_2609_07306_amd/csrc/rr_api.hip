@@ -296,11 +296,12 @@ rr::RouteArgs route_args(const rr_config &c, const void *Q, const void *K)
     return a;
 }
 
-// Schedule of a relay layer for a configuration: one pass where a tile's
-// ledger bitmaps fit its LDS -- by default unless the inputs are non-causal
-// and the rescoring would use dense tiles, whose threshold seeds make the
-// split schedule faster there -- and, for the split schedule with dense
-// rescoring, whether the rescoring pass leaves threshold seeds.
+// Schedule of a relay layer for a configuration: by default one pass for
+// causal inputs where a tile's ledger bitmaps fit its LDS (compaction would
+// mix short and long causal rows in one tile), else the split schedule,
+// measured faster for non-causal inputs with dense or gathered rescoring;
+// and, for the split schedule with dense rescoring, whether the rescoring
+// pass leaves threshold seeds.
 struct RelayPlan {
     bool fused, seeds;
     int bm_words;
@@ -313,8 +314,7 @@ RelayPlan relay_plan(const rr_config &c)
     p.bm_words = relay_bm_words(c.n_k);
     const bool fits = p.bm_words <= rr::route_relay_max_bm_words(c.dtype, c.d, c.k + c.m);
     rr::rescore_geometry(rows_of(c), c.n_q, c.n_k, p.geo);
-    p.fused = fits && ((c.options & RR_OPT_ONE_PASS_RELAY) ||
-                       (!(c.options & RR_OPT_SPLIT_RELAY) && (c.causal || !p.geo.dense)));
+    p.fused = fits && ((c.options & RR_OPT_ONE_PASS_RELAY) || (!(c.options & RR_OPT_SPLIT_RELAY) && c.causal));
     p.seeds = !p.fused && p.geo.dense && rr::rescore_dense_seeds(c.dtype, c.d);
     return p;
 }
