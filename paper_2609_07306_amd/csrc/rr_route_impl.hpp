@@ -668,8 +668,7 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
     __shared__ int32_t r_nc[BM], r_ns[BM];            // relay: the row's ledger counts |R|, |C|
     __shared__ int32_t s_last;
 
-    const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, hh = lane >> 5, l32 = lane & 31;
-    const int rb = w % NW, p = w / NW;  // row block and key split of this wave
+    const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;  // (each tile takes them afresh)
     constexpr int mode = MODE;  // one instance per caller
     const int T = a.k + a.m;
     const int group = a.n_heads / a.n_kv_heads;
@@ -920,8 +919,36 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
         // relay: the ledger rows -> per-row bitmaps over the key range, (R
         // word, C word) per 32 keys, in the candidate region (free until the
         // collection sweep).  Wave w reads rows w, w + NWV, ..., a lane per
-        // ledger slot; every lane loads (masked slots read row 0).
+        // ledger slot; every lane loads (masked slots read row 0).  The first
+        // chunk of ledger loads and then the query fragments are requested
+        // before the bitmap clear, whose barrier orders LDS only, so that
+        // both are in flight during it.
         uint2 *rbm = reinterpret_cast<uint2 *>(ss);
+        constexpr int RPW = BM / C::NWV;
+        static_assert(BM % C::NWV == 0, "rows split evenly over the waves");
+        const int c_led = a.k + c_sent;
+        int led_id[RPW];
+        auto load_led = [&](int s0) __attribute__((always_inline)) {
+            const int slot = s0 + lane;
+            const bool inr = slot < a.k, live = slot < c_led;
+            const int32_t *col = inr ? a.led_routes + slot : (live ? a.led_sent + (slot - a.k) : a.led_routes);
+            const int64_t stride = inr ? a.k : (live ? c_sent : a.k);
+#pragma unroll
+            for (int q = 0; q < RPW; ++q) {
+                const int64_t g = row_g[w + q * C::NWV];
+                const bool ok = live && g >= 0;
+                const int v = col[(ok ? g : 0) * stride];
+                led_id[q] = ok ? v : -1;
+            }
+        };
+        if constexpr (mode == MODE_RELAY) load_led(0);
+
+        Frag<DT, D> fq;
+        if (row_g[myrow] >= 0)
+            fq.load(reinterpret_cast<const DT *>(a.Q) + (int64_t)row_g[myrow] * D, hh);
+        else
+            fq.zero();
+
         if constexpr (mode == MODE_RELAY) {
             const int nwd = a.bm_words;
             for (int j = tid; j < BM * nwd; j += C::NT) rbm[j] = make_uint2(0u, 0u);
@@ -930,31 +957,19 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
                 s_tot_rows = 0;
             }
             lds_barrier();
-            constexpr int RPW = BM / C::NWV;
-            static_assert(BM % C::NWV == 0, "rows split evenly over the waves");
             int nc[RPW], ns[RPW];
 #pragma unroll
             for (int q = 0; q < RPW; ++q) nc[q] = ns[q] = 0;
             uint32_t *bw = reinterpret_cast<uint32_t *>(rbm);
-            const int c_led = a.k + c_sent;
             for (int s0 = 0; s0 < c_led; s0 += 64) {
-                const int slot = s0 + lane;
-                const bool inr = slot < a.k, live = slot < c_led;
-                const int32_t *col = inr ? a.led_routes + slot : (live ? a.led_sent + (slot - a.k) : a.led_routes);
-                const int64_t stride = inr ? a.k : (live ? c_sent : a.k);
-                int id[RPW];
-#pragma unroll
-                for (int q = 0; q < RPW; ++q) {
-                    const int64_t g = row_g[w + q * C::NWV];
-                    const bool ok = live && g >= 0;
-                    const int v = col[(ok ? g : 0) * stride];
-                    id[q] = ok ? v : -1;
-                }
+                if (s0 > 0) load_led(s0);
+                const bool inr = s0 + lane < a.k;
 #pragma unroll
                 for (int q = 0; q < RPW; ++q) {
                     const int r = w + q * C::NWV;
-                    const bool ok = id[q] >= 0 && id[q] < a.n_k;  // ledger ids lie in [0, n_i); -1 is an empty slot
-                    if (ok) atomicOr(&bw[2 * (r * nwd + (id[q] >> 5)) + (inr ? 0 : 1)], 1u << (id[q] & 31));
+                    const int id = led_id[q];
+                    const bool ok = id >= 0 && id < a.n_k;  // ledger ids lie in [0, n_i); -1 is an empty slot
+                    if (ok) atomicOr(&bw[2 * (r * nwd + (id >> 5)) + (inr ? 0 : 1)], 1u << (id & 31));
                     nc[q] += __popcll(__ballot(ok && inr));
                     ns[q] += __popcll(__ballot(ok && !inr));
                 }
@@ -968,12 +983,6 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
             }
             lds_barrier();
         }
-
-        Frag<DT, D> fq;
-        if (row_g[myrow] >= 0)
-            fq.load(reinterpret_cast<const DT *>(a.Q) + (int64_t)row_g[myrow] * D, hh);
-        else
-            fq.zero();
 
         // the collection sweep's key ring; its first two stages are requested
         // as soon as no other sweep needs the loads, so that they arrive
@@ -1325,7 +1334,7 @@ __global__ __launch_bounds__(64 * NW * KS) void route_kernel(RouteArgs a)
         int32_t *stg = reinterpret_cast<int32_t *>(bt);  // [BM][STG]: R at 0.., N at k..
         int32_t *s_nR = id_lo, *s_nN = id_hi;           // reused: staged R and N counts per row
         {
-            const int r = 16 * w + (lane & 15), qq = lane >> 4, l16 = lane & 15;
+            const int r = 16 * w + (lane & 15), qq = lane >> 4;
             if (row_g[r] >= 0) {  // the four lanes of a row take this branch together
                 const int64_t row = row_g[r];
                 const int c = rcnt[r];
